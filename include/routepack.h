@@ -1,0 +1,203 @@
+/*
+ * routepack.h -- C-ABI of the MI355X (gfx950) RoutePack planner hot path.
+ *
+ * RoutePack (arXiv 2608.12146) plans one optimizer-step window of a MoE RL
+ * trainer in three data-parallel stages, each exported here:
+ *   1. window demand aggregation and layer-local LPT expert placement
+ *      (Sec. 3.3, Alg. 1), plus the per-sample physical-rank demand
+ *      (Eq. physical-rank-demand);
+ *   2. the smallest feasible number of token-capped execution rows and a
+ *      feasible seed population (Eqs. sample-bijection .. min-row-count,
+ *      Alg. 2);
+ *   3. fixed-row population annealing over the DP layout of those rows
+ *      (Alg. 3) under the EDP-shard-aware lexicographic score
+ *      (Eqs. cell-token-statistics .. lexicographic-score).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Arrays are C-order and live in DEVICE memory unless marked [host].  The
+ *   caller owns every array; the library keeps no pointer after a call's
+ *   stream work completes and frees its own scratch before returning
+ *   (synchronous calls) or stream-ordered on `stream` (asynchronous calls).
+ * - Work is enqueued on the caller's `stream`.  Calls marked "synchronizes"
+ *   wait for that stream before returning.  There is no global mutable
+ *   state; calls on different streams are independent.
+ * - Layout encoding: a layout is int32 [N] holding, for each sample i, its
+ *   cell id c = r * D + d (row r in [0, R), DP slot d in [0, D)).  A
+ *   row-shard is h = r * G + g with g = dp_to_edp[d].
+ * - Fixed point: every cost is an int64 in units of 2^-F raw tokens; the
+ *   paper's normalised value is value / (2^F * C).  Score s = (s0, s1, s2) =
+ *   (max_g U_g, sum_g U_g, max_{r,g} J), ordered lexicographically.
+ * - Every function returns 0 or one of the negative ROUTEPACK_E_* codes;
+ *   on an error nothing is guaranteed about output arrays.
+ */
+#ifndef ROUTEPACK_H
+#define ROUTEPACK_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ROUTEPACK_OK             0
+#define ROUTEPACK_E_INVALID     -1  /* null pointer, bad size, E % P != 0, bad partition, C <= 0, bad schedule */
+#define ROUTEPACK_E_INFEASIBLE  -2  /* some t_i > C, t_i < 1, or floor(N / D) below the row lower bound */
+#define ROUTEPACK_E_HEURISTIC   -3  /* FixedRowFFD found no row count <= floor(N / D) */
+#define ROUTEPACK_E_LAYOUT      -4  /* an input layout violates Eqs. sample-bijection .. token-capacity */
+#define ROUTEPACK_E_OVERFLOW    -5  /* R*G*(A_max + E_max + 1) >= 2^53: scores not exact in int64/double */
+#define ROUTEPACK_E_DEVICE      -6  /* a HIP runtime error */
+#define ROUTEPACK_E_INTERNAL    -7  /* a postcondition failed (validation of x*, non-regression) */
+#define ROUTEPACK_E_UNSUPPORTED -8  /* a size this build's kernels do not handle (documented per call) */
+
+/* Problem description (Sec. 3.1-3.4).
+ * demand a[i][l][e] and lengths t_i are the routing-replay input (Eq.
+ * routing-replay-input); D DP slots are partitioned into G EDP shards by
+ * dp_to_edp (every shard non-empty); C is the token cap of one cell (Eq.
+ * token-capacity); stage s costs alpha_s * sum t + beta_s * sum t^2 raw
+ * tokens (Eq. attention-cost-proxy), given at scale 2^frac_bits; min_rows is
+ * an optional pipeline lower bound on R (Sec. 3.2), 1 for none. */
+typedef struct routepack_problem {
+    int32_t n_samples;        /* N >= 1 */
+    int32_t n_layers;         /* L >= 0 MoE layers */
+    int32_t n_experts;        /* E >= 1 logical experts per layer */
+    int32_t top_k;            /* k: informational */
+    int32_t n_ranks;          /* P >= 1 physical EP ranks; E % P == 0; H = E / P */
+    int32_t n_dp;             /* D >= 1 controller DP slots */
+    int32_t n_edp;            /* G in [1, D] EDP shards */
+    const int32_t *dp_to_edp; /* [host][D] shard of each slot */
+    int64_t capacity;         /* C >= 1 tokens per cell */
+    int32_t n_stages;         /* S >= 1 attention stages */
+    const int64_t *alpha_fp;  /* [host][S] >= 0, a_s * 2^frac_bits */
+    const int64_t *beta_fp;   /* [host][S] >= 0, b_s * 2^frac_bits */
+    int32_t frac_bits;        /* F in [0, 30] */
+    int32_t min_rows;         /* >= 1 */
+} routepack_problem;
+
+/* Window demand aggregation (Sec. 3.3): agg[l][e] = sum_i demand[i][l][e],
+ * exact in int64.
+ *   demand  int32 [N][L][E]   replayed routing counts, >= 0
+ *   agg     int64 [L][E]      out
+ * Asynchronous.  E_INVALID on null pointers or negative sizes. */
+int routepack_aggregate_demand(const routepack_problem *prob, const int32_t *demand,
+                               int64_t *agg, hipStream_t stream);
+
+/* Layer-local LPT placement (Alg. 1), every layer independently: experts by
+ * (-agg, e), each to the rank with fewer than H experts minimising
+ * (G_p, p), taking slot p*H + n_p.  owner(v) = v / H.
+ *   agg         int64 [L][E]          window aggregate
+ *   slot_of     int32 [L][E]          out: pi_l(e)
+ *   rank_load   int64 [L][P]          out: G_{l,p} (Eq. placement-load)
+ *   demand      int32 [N][L][E] or NULL
+ *   q           int32 [N][L][P] or NULL  out: q[i][l][p] = sum over e with
+ *               owner(pi_l(e)) = p of demand[i][l][e] (Eq. physical-rank-demand);
+ *               computed only when both demand and q are given.
+ * Asynchronous.  E_INVALID on null outputs or E % P != 0. */
+int routepack_place_experts(const routepack_problem *prob, const int64_t *agg,
+                            int32_t *slot_of, int64_t *rank_load,
+                            const int32_t *demand, int32_t *q, hipStream_t stream);
+
+/* Row count and seed population (Sec. 3.2 and Alg. 2).
+ * R_lb = max(1, min_rows, ceil(sum t / (C D)), ceil(#{t_i > C/2} / D));
+ * R* = the first R >= R_lb for which FixedRowFFD with R*D cells succeeds
+ * (the R*D longest samples by (-t, i) open the cells, every later one goes
+ * to the lowest-index cell with room); certified = (R* == R_lb).  Seeds:
+ * x_length (FFD), x_paired (EDPAwarePair of its cells, width 1, kept only if
+ * strictly better), then n_trials - 2 randomized trials (WindowShuffle,
+ * RandomizedBestFit, EDPAwarePair with width choice_width; Philox4x64-10
+ * key (seed, 0), counter (draw, trial, phase, 3)); each in canonical form,
+ * duplicates dropped, ordered by (score, discovery) and repeated cyclically
+ * into pop_size members.
+ *   lengths     int32 [N]            t_i in [1, C]
+ *   q           int32 [N][L][P]      physical-rank demand
+ *   r_star      [host] int32 out
+ *   certified   [host] int32 out     1 when R* equals the lower bound
+ *   population  int32 [pop_size][N]  out: canonical layouts
+ *   scores      int64 [pop_size][3]  out
+ *   info        [host] int32 [3] out or NULL: {R_lb, distinct seeds, trials kept}
+ * Synchronizes.  E_INFEASIBLE, E_HEURISTIC, E_OVERFLOW as above;
+ * E_UNSUPPORTED when L*P > 4096 or R*D > 4096. */
+int routepack_pack_rows(const routepack_problem *prob, const int32_t *lengths, const int32_t *q,
+                        uint64_t seed, int32_t n_trials, int32_t choice_width, int32_t pop_size,
+                        int32_t *r_star, int32_t *certified, int32_t *population,
+                        int64_t *scores, int32_t *info, hipStream_t stream);
+
+/* Annealing schedule and proposal knobs (Sec. 4.1.2, Alg. 3). */
+typedef struct routepack_anneal_params {
+    int32_t n_sweeps;            /* temperature levels in this call, >= 0 */
+    int32_t steps_per_sweep;     /* K proposal steps per member per level, >= 0 */
+    const double *temperatures;  /* [host][n_sweeps] > 0, strictly decreasing */
+    double t_next;               /* temperature of the level after this call (< last);
+                                    <= 0 when this call ends the schedule (no resampling
+                                    after its last level) */
+    uint32_t p_guide_u32;        /* guided branch iff lo32(w0) < p_guide_u32 (0.8 -> 0xCCCCCCCD) */
+    uint32_t rho_u32;            /* relocation iff hi32(w0) < rho_u32 (0.25 -> 0x40000000) */
+    uint64_t seed;               /* Philox4x64-10 key (seed, 0) */
+    int32_t sweep_offset;        /* global index of this call's first level */
+    int32_t init_incumbent;      /* 1: x* := lowest-index argmin of the population */
+} routepack_anneal_params;
+
+/* Fixed-row population annealing (Alg. 3) over n_sweeps levels.  Level n
+ * (global index nn = sweep_offset + n) runs, for every member j independently,
+ * K steps of: GuidedProposal (Sec. 4.1.2) with Philox words from counters
+ * (k, nn, j, 0) and (k, nn, j, 1); a feasibility test (distinct cells,
+ * capacity, no emptied cell) -- an infeasible proposal consumes the step;
+ * IncrementalScore; the Metropolis test "s' < s lexicographically, or
+ * u < exp(-max(Delta, 0) / T_n)" on the energy of Eq. pa-energy; and the
+ * trajectory best (strict improvement).  After the level the incumbent x*
+ * takes the lexicographic minimum of itself and every trajectory best
+ * (strict, ascending j) and, unless the level is the schedule's last, the
+ * terminal states are resampled systematically with Boltzmann weights for
+ * the temperature change.  Moves never change R, coverage, capacity or the
+ * shard topology.  Resuming with (population, x*, sweep_offset) is exact.
+ *   lengths      int32 [N]
+ *   q            int32 [N][L][P]
+ *   n_rows       R (the fixed row count)
+ *   population   int32 [pop_size][N]  in: start of level sweep_offset; out: start of
+ *                the next level (resampled) or the terminal states (t_next <= 0)
+ *   best_layout  int32 [N]    in/out x* (ignored on input when init_incumbent)
+ *   best_score   int64 [3]    in/out Score(x*)
+ *   trace        int64 [n_sweeps][pop_size][8] out or NULL: terminal score (3),
+ *                trajectory-best score (3), accepted steps, evaluated steps
+ *   parents      int32 [n_sweeps][pop_size] out or NULL: parent of each member
+ *                after the level, -1 when no resampling followed it
+ *   step_log     uint8 [n_sweeps][pop_size][K] out or NULL: 0 infeasible,
+ *                1 rejected, 2 accepted
+ * Synchronizes.  E_LAYOUT when a population member (or the given x*) is not
+ * feasible for R or best_score does not match x*; E_INTERNAL when the final
+ * validation or the non-regression check fails; E_UNSUPPORTED when P is not
+ * a power of two <= 64, L*P > 4096, or R*G > 4096. */
+int routepack_anneal(const routepack_problem *prob, const int32_t *lengths, const int32_t *q,
+                     int32_t n_rows, int32_t pop_size, int32_t *population,
+                     const routepack_anneal_params *params, int32_t *best_layout,
+                     int64_t *best_score, int64_t *trace, int32_t *parents, uint8_t *step_log,
+                     hipStream_t stream);
+
+/* Exact objective of many layouts (Eqs. cell-token-statistics ..
+ * lexicographic-score) with validation and the online load diagnostics of
+ * Sec. 6.3 (Eqs. global-ep-cv and ep-efficiency).
+ *   layouts    int32 [n_layouts][N]
+ *   scores     int64 [n_layouts][3]  out (INT64_MAX x3 for an invalid layout)
+ *   status     int32 [n_layouts]     out: 0, or bit 0 a cell id outside [0, R*D),
+ *              bit 1 a cell over capacity, bit 2 an empty cell
+ *   J          int64 [n_layouts][R*G] out or NULL: J per row-shard
+ *   diag       double [n_layouts][8] out or NULL: CV_global (NaN without
+ *              rank_load), S_EP, T_EP (raw tokens), eta_EP, sum A, max_g U,
+ *              sum_g U (normalised by C), energy (Eq. pa-energy)
+ *   rank_load  int64 [L][P] or NULL: window rank load for CV_global
+ * Synchronizes (it sizes its scratch from a bound computed on the device).
+ * E_OVERFLOW as above. */
+int routepack_eval_objective(const routepack_problem *prob, const int32_t *lengths,
+                             const int32_t *q, int32_t n_rows, int32_t n_layouts,
+                             const int32_t *layouts, int64_t *scores, int32_t *status,
+                             int64_t *J, double *diag, const int64_t *rank_load,
+                             hipStream_t stream);
+
+/* Human-readable name of a status code. */
+const char *routepack_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ROUTEPACK_H */

@@ -1,0 +1,228 @@
+"""GPU vs oracle parity through the C-ABI (bit-exact for every integer
+result; float diagnostics to a relative 1e-6).
+
+Windows are the seeded synthetic stand-ins for routing-replay traces; the
+oracle runs on the same inputs.  Full trajectories are compared on the small
+windows; on the larger ones the GPU runs the bench's launch configuration and
+sampled levels are recomputed by the oracle from the GPU's own start
+population (every level of every member is an independent chain given its
+start state, the seed and the level index).
+"""
+import functools
+import os
+
+import numpy as np
+import pytest
+
+import synth
+
+gpu = pytest.mark.gpu
+DIAG_RTOL = 1e-6
+
+
+def _log(msg):
+    print(f"[gpu-parity] {msg}", flush=True)
+
+
+@functools.lru_cache(maxsize=None)
+def _window(name, G=1):
+    import oracle as O
+    w = synth.make_window(name, edp=G)
+    pd = synth.window_problem(w)
+    pb = O.Problem.from_dict(pd)
+    agg = O.aggregate(w.demand)
+    slot, load = O.place(agg, w.n_ranks)
+    q = O.project(w.demand, slot, w.n_ranks)
+    return w, pd, pb, agg, slot, load, q
+
+
+@functools.lru_cache(maxsize=None)
+def _packed(name, G=1):
+    import oracle as O
+    w, pd, pb, agg, slot, load, q = _window(name, G)
+    pr = O.pack_rows(pb, w.lengths, q, w.seed_pack, synth.windows.N_TRIALS,
+                     synth.windows.CHOICE_WIDTH, w.pop)
+    assert pr["rc"] == 0
+    return pr
+
+
+def _rp():
+    import paper_2608_12146_amd as rp
+    return rp
+
+
+@gpu
+@pytest.mark.parametrize("name", ["tiny", "small", "mid", "heavy"])
+def test_aggregate_place_project(name):
+    rp = _rp()
+    _log(f"aggregate/place/project {name}")
+    w, pd, pb, agg, slot, load, q = _window(name)
+    prob = rp.Problem.from_dict(pd)
+    g_agg = rp.aggregate_demand(prob, w.demand)
+    assert np.array_equal(g_agg.cpu().numpy(), agg)
+    g_slot, g_load, g_q = rp.place_experts(prob, g_agg, w.demand)
+    assert np.array_equal(g_slot.cpu().numpy(), slot)
+    assert np.array_equal(g_load.cpu().numpy(), load)
+    assert np.array_equal(g_q.cpu().numpy(), q)
+
+
+@gpu
+def test_aggregate_ragged_and_unaligned():
+    rp = _rp()
+    rng = np.random.default_rng(0)
+    for (n, L, E) in [(1, 1, 1), (3, 5, 7), (1000, 3, 13), (257, 2, 6)]:
+        d = rng.integers(0, 1000, size=(n, L, E)).astype(np.int32)
+        prob = rp.Problem(n, L, E, 1, 1, 1, 1, [0], 10**6, [4096], [1])
+        g = rp.aggregate_demand(prob, d)
+        assert np.array_equal(g.cpu().numpy(), d.sum(axis=0, dtype=np.int64))
+
+
+@gpu
+@pytest.mark.parametrize("name,G", [("tiny", 1), ("tiny", 2), ("small", 1), ("small", 4), ("mid", 1)])
+def test_eval_objective(name, G):
+    import oracle as O
+    rp = _rp()
+    _log(f"eval_objective {name} G={G}")
+    w, pd, pb, agg, slot, load, q = _window(name, G)
+    pr = _packed(name, G)
+    R = pr["r_star"]
+    lays = pr["population"][: min(w.pop, 32)].copy()
+    # add infeasible layouts: an out-of-range id and an over-full cell
+    bad1 = lays[0].copy(); bad1[0] = R * w.n_dp
+    lays = np.concatenate([lays, bad1[None]])
+    prob = rp.Problem.from_dict(pd)
+    out = rp.eval_objective(prob, w.lengths, q, R, lays, rank_load=load, want_J=True, want_diag=True)
+    sc, st, J, dg = (out[k].cpu().numpy() for k in ("scores", "status", "J", "diag"))
+    for m in range(len(lays)):
+        ost, os_, oJ, odg = O.score(pb, w.lengths, q, R, lays[m], rank_load=load, want_J=True, want_diag=True)
+        assert st[m] == ost
+        assert sc[m].tolist() == os_.tolist()
+        assert J[m].tolist() == oJ.tolist()
+        if ost == 0:
+            np.testing.assert_allclose(dg[m], odg, rtol=DIAG_RTOL, atol=0)
+
+
+def _compare_anneal(g, o, steps=False):
+    assert np.array_equal(g["trace"].cpu().numpy(), o["trace"])
+    assert np.array_equal(g["parents"].cpu().numpy(), o["parents"])
+    assert np.array_equal(g["population"].cpu().numpy(), o["population"])
+    assert np.array_equal(g["best_layout"].cpu().numpy(), o["best_layout"])
+    assert np.array_equal(g["best_score"].cpu().numpy(), o["best_score"])
+    if steps:
+        assert np.array_equal(g["steps"].cpu().numpy(), o["steps"])
+
+
+@gpu
+@pytest.mark.parametrize("G", [1, 2])
+def test_anneal_full_trajectory_tiny(G):
+    import oracle as O
+    rp = _rp()
+    _log(f"anneal tiny G={G} full schedule")
+    w, pd, pb, agg, slot, load, q = _window("tiny", G)
+    pr = _packed("tiny", G)
+    temps = synth.anneal_temperatures(w.levels)
+    K = synth.windows.STEPS_PER_LEVEL
+    o = O.anneal(pb, w.lengths, q, pr["r_star"], pr["population"], temps, K, w.seed_anneal,
+                 want_steps=True)
+    assert o["rc"] == 0
+    g = rp.anneal(rp.Problem.from_dict(pd), w.lengths, q, pr["r_star"], pr["population"], temps, K,
+                  w.seed_anneal, want_steps=True)
+    _compare_anneal(g, o, steps=True)
+
+
+@gpu
+@pytest.mark.parametrize("G", [1, 4])
+def test_anneal_small_levels(G):
+    import oracle as O
+    rp = _rp()
+    w, pd, pb, agg, slot, load, q = _window("small", G)
+    pr = _packed("small", G)
+    temps = synth.anneal_temperatures(w.levels)[:40]
+    K = synth.windows.STEPS_PER_LEVEL
+    _log(f"anneal small G={G} 40 levels")
+    o = O.anneal(pb, w.lengths, q, pr["r_star"], pr["population"], temps, K, w.seed_anneal,
+                 t_next=synth.anneal_temperatures(w.levels)[40])
+    assert o["rc"] == 0
+    g = rp.anneal(rp.Problem.from_dict(pd), w.lengths, q, pr["r_star"], pr["population"], temps, K,
+                  w.seed_anneal, t_next=synth.anneal_temperatures(w.levels)[40])
+    _compare_anneal(g, o)
+
+
+@gpu
+def test_anneal_mid_sampled_levels():
+    """Mid window at its full population: two levels from the seeds, then one
+    late level resumed from the GPU's population, each checked against the
+    oracle on the same start states."""
+    import oracle as O
+    rp = _rp()
+    w, pd, pb, agg, slot, load, q = _window("mid")
+    pr = _packed("mid")
+    temps = synth.anneal_temperatures(w.levels)
+    K = synth.windows.STEPS_PER_LEVEL
+    prob = rp.Problem.from_dict(pd)
+    _log("anneal mid levels 0-1")
+    o = O.anneal(pb, w.lengths, q, pr["r_star"], pr["population"], temps[:2], K, w.seed_anneal,
+                 t_next=temps[2])
+    g = rp.anneal(prob, w.lengths, q, pr["r_star"], pr["population"], temps[:2], K, w.seed_anneal,
+                  t_next=temps[2])
+    _compare_anneal(g, o)
+    _log("anneal mid level 1500 resumed")
+    start = g["population"].cpu().numpy()
+    o2 = O.anneal(pb, w.lengths, q, pr["r_star"], start, temps[1500:1501], K, w.seed_anneal,
+                  t_next=temps[1501], sweep_offset=1500, best_layout=o["best_layout"],
+                  best_score=o["best_score"])
+    g2 = rp.anneal(prob, w.lengths, q, pr["r_star"], start, temps[1500:1501], K, w.seed_anneal,
+                   t_next=temps[1501], sweep_offset=1500, best_layout=g["best_layout"],
+                   best_score=g["best_score"])
+    _compare_anneal(g2, o2)
+
+
+@gpu
+def test_anneal_resume_is_exact_on_gpu():
+    rp = _rp()
+    w, pd, pb, agg, slot, load, q = _window("tiny")
+    pr = _packed("tiny")
+    temps = synth.anneal_temperatures(30)
+    prob = rp.Problem.from_dict(pd)
+    full = rp.anneal(prob, w.lengths, q, pr["r_star"], pr["population"], temps, 64, 9)
+    a = rp.anneal(prob, w.lengths, q, pr["r_star"], pr["population"], temps[:11], 64, 9, t_next=temps[11])
+    b = rp.anneal(prob, w.lengths, q, pr["r_star"], a["population"], temps[11:], 64, 9, sweep_offset=11,
+                  best_layout=a["best_layout"], best_score=a["best_score"])
+    assert np.array_equal(full["population"].cpu().numpy(), b["population"].cpu().numpy())
+    assert np.array_equal(full["best_layout"].cpu().numpy(), b["best_layout"].cpu().numpy())
+    import torch
+    assert torch.equal(full["trace"], torch.cat([a["trace"], b["trace"]]))
+
+
+@gpu
+def test_anneal_deterministic_reruns():
+    rp = _rp()
+    w, pd, pb, agg, slot, load, q = _window("small")
+    pr = _packed("small")
+    temps = synth.anneal_temperatures(w.levels)[:10]
+    prob = rp.Problem.from_dict(pd)
+    ref = rp.anneal(prob, w.lengths, q, pr["r_star"], pr["population"], temps, 256, 5, t_next=1e-5)
+    for _ in range(3):
+        g = rp.anneal(prob, w.lengths, q, pr["r_star"], pr["population"], temps, 256, 5, t_next=1e-5)
+        assert np.array_equal(g["trace"].cpu().numpy(), ref["trace"].cpu().numpy())
+        assert np.array_equal(g["population"].cpu().numpy(), ref["population"].cpu().numpy())
+
+
+@gpu
+def test_anneal_error_paths():
+    rp = _rp()
+    w, pd, pb, agg, slot, load, q = _window("tiny")
+    pr = _packed("tiny")
+    prob = rp.Problem.from_dict(pd)
+    bad = pr["population"].copy()
+    bad[0, 0] = pr["r_star"] * w.n_dp          # cell id out of range
+    with pytest.raises(rp.RoutepackError) as ei:
+        rp.anneal(prob, w.lengths, q, pr["r_star"], bad, [1e-3], 8, 1)
+    assert ei.value.code == -4
+    with pytest.raises(rp.RoutepackError) as ei:     # increasing temperatures
+        rp.anneal(prob, w.lengths, q, pr["r_star"], pr["population"], [1e-3, 2e-3], 8, 1)
+    assert ei.value.code == -1
+    with pytest.raises(rp.RoutepackError) as ei:     # x* that does not carry its score
+        rp.anneal(prob, w.lengths, q, pr["r_star"], pr["population"], [1e-3], 8, 1,
+                  best_layout=pr["population"][0], best_score=np.array([1, 2, 3]))
+    assert ei.value.code == -4

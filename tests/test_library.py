@@ -1,0 +1,44 @@
+"""Host-side checks of the C-ABI library that need no GPU: it loads and
+exports every entry point include/routepack.h declares, and argument errors
+are reported before any device work."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "routepack.h")).read()
+    return sorted(set(re.findall(r"^(?:int|const char \*)\s*(routepack_\w+)\s*\(", src, re.M)))
+
+
+def test_header_declares_the_boundary():
+    assert _declared() == sorted(["routepack_aggregate_demand", "routepack_place_experts",
+                                  "routepack_pack_rows", "routepack_anneal",
+                                  "routepack_eval_objective", "routepack_strerror"])
+
+
+def test_library_exports_every_declared_symbol():
+    import paper_2608_12146_amd as rp
+    lib = rp.load_library()
+    for name in _declared():
+        assert hasattr(lib, name), name
+    assert lib.routepack_strerror(-5) == b"fixed-point score bound exceeds 2^53"
+
+
+def test_invalid_problems_rejected_without_device_work():
+    import paper_2608_12146_amd as rp
+    lib = rp.load_library()
+    # E % P != 0 and a shard with no slot: rejected during validation.
+    bad = rp.Problem(8, 2, 6, 2, 4, 2, 1, [0, 0], 64, [4096], [1])
+    assert lib.routepack_eval_objective(bad.ref, None, None, 1, 0, None, None, None, None, None,
+                                        None, None) == -1
+    bad2 = rp.Problem(8, 2, 8, 2, 4, 2, 2, [0, 0], 64, [4096], [1])
+    assert lib.routepack_anneal(bad2.ref, None, None, 1, 1, None, None, None, None, None, None,
+                                None, None) == -1
+    assert lib.routepack_place_experts(bad.ref, None, None, None, None, None, None) == -1
+    assert lib.routepack_aggregate_demand(None, None, None, None) == -1
