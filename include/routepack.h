@@ -136,6 +136,8 @@ typedef struct routepack_anneal_params {
     uint64_t seed;               /* Philox4x64-10 key (seed, 0) */
     int32_t sweep_offset;        /* global index of this call's first level */
     int32_t init_incumbent;      /* 1: x* := lowest-index argmin of the population */
+    double *level_kernel_ms;     /* [host][n_sweeps] out or NULL: duration of each level's
+                                    annealing kernel, from HIP events on `stream` */
 } routepack_anneal_params;
 
 /* Fixed-row population annealing (Alg. 3) over n_sweeps levels.  Level n

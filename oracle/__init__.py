@@ -203,7 +203,7 @@ def resample(energies, t_cur, t_next, seed, level):
 def anneal(prob: Problem, lengths, q, n_rows, population, temperatures, steps_per_sweep, seed,
            t_next=0.0, sweep_offset=0, p_guide_u32=0xCCCCCCCD, rho_u32=0x40000000,
            best_layout=None, best_score=None, want_trace=True, want_parents=True,
-           want_steps=False, n_threads=None, check_full=False):
+           want_steps=False, n_threads=None, check_full=False, replica_ids=None):
     """Population annealing (Alg. 3) over len(temperatures) levels.
     Returns dict(rc, population, best_layout, best_score, trace, parents, steps)."""
     lib = _load()
@@ -222,13 +222,16 @@ def anneal(prob: Problem, lengths, q, n_rows, population, temperatures, steps_pe
     ap = _AnnealParams(ns, steps_per_sweep, _p(temps, C.c_double), float(t_next), p_guide_u32,
                        rho_u32, seed, sweep_offset, 1 if init else 0)
     if n_threads is None:
-        n_threads = min(P, os.cpu_count() or 1)
+        n_threads = min(P, os.cpu_count() or 1, 16)
+    rid = None if replica_ids is None else np.ascontiguousarray(replica_ids, dtype=np.int32)
+    assert rid is None or rid.shape == (P,)
     rc = lib.or_anneal(prob.ref, _p(t, C.c_int32), _p(qq, C.c_int32), C.c_int32(n_rows),
                        C.c_int32(P), _p(popl, C.c_int32), C.byref(ap), _p(bl, C.c_int32),
                        _p(bs, C.c_int64),
                        _p(trace, C.c_int64) if trace is not None else None,
                        _p(parents, C.c_int32) if parents is not None else None,
                        _p(steps, C.c_uint8) if steps is not None else None,
-                       C.c_int32(n_threads), C.c_int32(1 if check_full else 0))
+                       C.c_int32(n_threads), C.c_int32(1 if check_full else 0),
+                       _p(rid, C.c_int32) if rid is not None else None)
     return dict(rc=rc, population=popl, best_layout=bl, best_score=bs, trace=trace,
                 parents=parents, steps=steps, n_threads=n_threads)

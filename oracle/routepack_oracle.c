@@ -356,21 +356,41 @@ done:
 }
 
 /* ------------------------------------------------------------------------ */
-/* Bound check: with capacity C and the largest per-layer window demand Wb,
- * every J is at most Ab + Eb, Ab = sum_s (alpha_s C + beta_s C^2),
- * Eb = 2^F L Wb, and R*G*(Ab+Eb+1) must stay below 2^53 so every score
- * component is exact in int64 and in a double. */
-static int overflow_check(const or_problem *pb, const int32_t *q, int32_t R, int64_t *wb_out)
+/* Bound check.  Every W entry of a capacity-feasible layout is at most
+ * Wb = min(max_l sum_{i,p} q[i][l][p], rate * maxD * C), where rate =
+ * max_i ceil(max_{l,p} q[i][l][p] / t_i) and maxD is the largest shard: the
+ * samples of one row-shard hold at most maxD * C tokens.  Then every J is at
+ * most Ab + Eb with Ab = sum_s (alpha_s C + beta_s C^2), Eb = 2^F L Wb, and
+ * R*G*(Ab+Eb+1) must stay below 2^53 so every score component is exact in
+ * int64 and in a double. */
+static int overflow_check(const or_problem *pb, const int32_t *t, const int32_t *q, int32_t R,
+                          int64_t *wb_out)
 {
     int32_t N = pb->n_samples, L = pb->n_layers, P = pb->n_ranks;
     long double lim = 9007199254740992.0L; /* 2^53 */
-    int64_t wb = 0;
+    int64_t wb = 0, rate = 0;
     for (int32_t l = 0; l < L; ++l) {
         int64_t tot = 0;
         for (int32_t i = 0; i < N; ++i)
             for (int32_t p = 0; p < P; ++p) tot += q[((int64_t)i * L + l) * P + p];
         if (tot > wb) wb = tot;
     }
+    for (int32_t i = 0; i < N; ++i) {
+        int64_t mx = 0;
+        for (int64_t x = 0; x < (int64_t)L * P; ++x)
+            if (q[(int64_t)i * L * P + x] > mx) mx = q[(int64_t)i * L * P + x];
+        int64_t r = t[i] > 0 ? (mx + t[i] - 1) / t[i] : mx;
+        if (r > rate) rate = r;
+    }
+    int32_t maxd = 0;
+    {
+        int32_t *cnt = calloc(pb->n_edp, sizeof(int32_t));
+        for (int32_t d = 0; d < pb->n_dp; ++d) cnt[pb->dp_to_edp[d]]++;
+        for (int32_t g = 0; g < pb->n_edp; ++g) if (cnt[g] > maxd) maxd = cnt[g];
+        free(cnt);
+    }
+    long double wcap = (long double)rate * maxd * (long double)pb->capacity;
+    if (wcap < (long double)wb) wb = (int64_t)wcap;
     long double C = (long double)pb->capacity;
     long double ab = 0.0L;
     for (int32_t s = 0; s < pb->n_stages; ++s)
@@ -704,7 +724,7 @@ int or_pack_rows(const or_problem *pb, const int32_t *t, const int32_t *q, uint6
     for (int64_t r = r_lb; r <= r_max; ++r)
         if (fixed_row_ffd(N, t, C, r * D, sigma, x_len)) { R = r; break; }
     if (R < 0) { free(sigma); free(x_len); return OR_HEURISTIC; }
-    if ((rc = overflow_check(pb, q, (int32_t)R, NULL))) { free(sigma); free(x_len); return rc; }
+    if ((rc = overflow_check(pb, t, q, (int32_t)R, NULL))) { free(sigma); free(x_len); return rc; }
     *r_star = (int32_t)R;
     *certified = (R == r_lb);
     topo_t tp;
@@ -1072,6 +1092,7 @@ typedef struct {
     int32_t *layouts;        /* [pop][N] in: start states, out: terminal states */
     chain_result *res;
     int check_full;
+    const int32_t *replica_ids;  /* member j runs the chain of replica replica_ids[j] */
 } worker_arg;
 
 static void *worker(void *p)
@@ -1081,7 +1102,8 @@ static void *worker(void *p)
     for (int32_t j = a->tid; j < a->pop; j += a->nthreads) {
         chain_t ch;
         chain_init(a->cx, &ch, a->layouts + (size_t)j * N);
-        run_chain(a->cx, &ch, a->ap, a->level, j, a->temp, &a->res[j], a->check_full);
+        int32_t rid = a->replica_ids ? a->replica_ids[j] : j;
+        run_chain(a->cx, &ch, a->ap, a->level, rid, a->temp, &a->res[j], a->check_full);
         memcpy(a->layouts + (size_t)j * N, ch.cell_of, sizeof(int32_t) * N);
         chain_free(a->cx, &ch);
     }
@@ -1131,11 +1153,13 @@ void or_resample(int32_t pop, const double *energies, double t_cur, double t_nex
  *   accepted count, evaluated count.  parents[n_sweeps][pop] (optional):
  *   parent of each member after the level (or -1 when no resampling).
  * step_log[n_sweeps][pop][K] (optional): 0 infeasible, 1 rejected, 2 accepted.
- * check_full: assert incremental == full rescore after every accepted step. */
+ * check_full: assert incremental == full rescore after every accepted step.
+ * replica_ids (optional): member j draws the random stream of replica
+ *   replica_ids[j] -- lets a subset of a large population be recomputed. */
 int or_anneal(const or_problem *pb, const int32_t *t, const int32_t *q, int32_t R, int32_t pop,
               int32_t *population, const or_anneal_params *ap, int32_t *best_layout,
               int64_t *best_score, int64_t *trace, int32_t *parents, uint8_t *step_log,
-              int32_t n_threads, int32_t check_full)
+              int32_t n_threads, int32_t check_full, const int32_t *replica_ids)
 {
     int rc = check_problem(pb);
     if (rc) return rc;
@@ -1146,7 +1170,7 @@ int or_anneal(const or_problem *pb, const int32_t *t, const int32_t *q, int32_t 
     }
     if (ap->n_sweeps > 0 && ap->t_next > 0.0 && !(ap->t_next < ap->temperatures[ap->n_sweeps - 1]))
         return OR_INVALID;
-    if ((rc = overflow_check(pb, q, R, NULL))) return rc;
+    if ((rc = overflow_check(pb, t, q, R, NULL))) return rc;
     int32_t N = pb->n_samples;
     topo_t tp;
     topo_build(pb, &tp);
@@ -1187,7 +1211,8 @@ int or_anneal(const or_problem *pb, const int32_t *t, const int32_t *q, int32_t 
         for (int32_t j = 0; j < pop; ++j)
             res[j].step_log = step_log ? step_log + ((size_t)n * pop + j) * K : NULL;
         for (int32_t x = 0; x < n_threads; ++x) {
-            wa[x] = (worker_arg){&cx, ap, level, pop, x, n_threads, ap->temperatures[n], terminal, res, check_full};
+            wa[x] = (worker_arg){&cx, ap, level, pop, x, n_threads, ap->temperatures[n], terminal, res,
+                                 check_full, replica_ids};
             pthread_create(&th[x], NULL, worker, &wa[x]);
         }
         for (int32_t x = 0; x < n_threads; ++x) pthread_join(th[x], NULL);

@@ -43,7 +43,8 @@ class _AnnealParams(C.Structure):
     _fields_ = [("n_sweeps", C.c_int32), ("steps_per_sweep", C.c_int32),
                 ("temperatures", C.POINTER(C.c_double)), ("t_next", C.c_double),
                 ("p_guide_u32", C.c_uint32), ("rho_u32", C.c_uint32), ("seed", C.c_uint64),
-                ("sweep_offset", C.c_int32), ("init_incumbent", C.c_int32)]
+                ("sweep_offset", C.c_int32), ("init_incumbent", C.c_int32),
+                ("level_kernel_ms", C.POINTER(C.c_double))]
 
 
 _lib = None
@@ -175,7 +176,7 @@ def pack_rows(prob: Problem, lengths, q, seed, n_trials, width, pop):
 def anneal(prob: Problem, lengths, q, n_rows, population, temperatures, steps_per_sweep, seed,
            t_next=0.0, sweep_offset=0, p_guide_u32=0xCCCCCCCD, rho_u32=0x40000000,
            best_layout=None, best_score=None, want_trace=True, want_parents=True, want_steps=False,
-           inplace=False):
+           inplace=False, kernel_times=False):
     """Population annealing; returns dict(population, best_layout, best_score, trace, parents, steps)."""
     torch = _torch()
     lib = load_library()
@@ -193,12 +194,15 @@ def anneal(prob: Problem, lengths, q, n_rows, population, temperatures, steps_pe
     trace = torch.empty((ns, P, 8), dtype=torch.int64, device="cuda") if want_trace else None
     parents = torch.empty((ns, P), dtype=torch.int32, device="cuda") if want_parents else None
     steps = torch.empty((ns, P, steps_per_sweep), dtype=torch.uint8, device="cuda") if want_steps else None
+    kms = np.zeros(max(ns, 1), dtype=np.float64) if kernel_times else None
     ap = _AnnealParams(ns, steps_per_sweep, temps.ctypes.data_as(C.POINTER(C.c_double)), float(t_next),
-                       p_guide_u32, rho_u32, seed, sweep_offset, 1 if init else 0)
+                       p_guide_u32, rho_u32, seed, sweep_offset, 1 if init else 0,
+                       kms.ctypes.data_as(C.POINTER(C.c_double)) if kms is not None else None)
     rc = lib.routepack_anneal(prob.ref, _ptr(t), _ptr(qq), n_rows, P, _ptr(popl), C.byref(ap), _ptr(bl),
                               _ptr(bs), _ptr(trace), _ptr(parents), _ptr(steps), _stream())
     _check("routepack_anneal", rc)
-    return dict(population=popl, best_layout=bl, best_score=bs, trace=trace, parents=parents, steps=steps)
+    return dict(population=popl, best_layout=bl, best_score=bs, trace=trace, parents=parents, steps=steps,
+                level_kernel_ms=None if kms is None else kms[:ns])
 
 
 def eval_objective(prob: Problem, lengths, q, n_rows, layouts, rank_load=None, want_J=False,

@@ -555,16 +555,63 @@ __global__ void __launch_bounds__(kThreads) k_anneal_level(AnnealArgs a) {
     }
 }
 
-// Builds member j's slab from its layout (cell ids): cell statistics, the
-// sorted member pool, the W rows and J/A of every row-shard.  status[j] gets
-// bit 0 for a cell id out of range, bit 1 for a cell over capacity, bit 2 for
-// an empty cell.  results[j][0..2] receive the member's score.
-__global__ void __launch_bounds__(kThreads) k_anneal_build(AnnealArgs a, const int32_t *layouts,
-                                                           int32_t *status) {
+// Building the member slabs from the start layouts.  Identical layouts are
+// built once: k_layout_hash hashes every layout (an order-free sum of a
+// 64-bit mix of (sample, cell)), k_leader finds for each member the first
+// member with an equal layout (hash match confirmed element by element),
+// and only those leaders are built; duplicates copy the leader's slab.
+__device__ inline uint64_t mix64(uint64_t z) {
+    z += 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+__global__ void __launch_bounds__(kThreads) k_layout_hash(const int32_t *layouts, int32_t N, uint64_t *hash) {
+    __shared__ uint64_t part[kThreads / kWave];
+    const int m = blockIdx.x;
+    const int32_t *lay = layouts + (int64_t)m * N;
+    uint64_t h = 0;
+    for (int32_t i = threadIdx.x; i < N; i += kThreads)
+        h += mix64(((uint64_t)(uint32_t)i << 32) | (uint32_t)lay[i]);
+    h = (uint64_t)wave_sum((int64_t)h);
+    if (lane_id() == 0) part[wave_id()] = h;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint64_t t = 0;
+        for (int w = 0; w < kThreads / kWave; ++w) t += part[w];
+        hash[m] = t;
+    }
+}
+
+__global__ void __launch_bounds__(64) k_leader(const int32_t *layouts, int32_t N, const uint64_t *hash,
+                                               int32_t *leader) {
+    const int m = blockIdx.x, lane = lane_id();
+    const int32_t *lay = layouts + (int64_t)m * N;
+    int32_t found = m;
+    for (int u = 0; u < m; ++u) {
+        if (hash[u] != hash[m]) continue;
+        const int32_t *o = layouts + (int64_t)u * N;
+        bool diff = false;
+        for (int32_t i = lane; i < N; i += kWave) diff |= (o[i] != lay[i]);
+        if (!__ballot(diff)) {
+            found = u;
+            break;
+        }
+    }
+    if (lane == 0) leader[m] = found;
+}
+
+// Cell statistics, validation, start offsets and the sorted member pool of
+// every leader.  status gets bit 0 for a cell id out of range, bit 1 for a
+// cell over capacity, bit 2 for an empty cell.
+__global__ void __launch_bounds__(kThreads) k_build_cells(AnnealArgs a, const int32_t *layouts,
+                                                          const int32_t *leader, int32_t *status) {
     extern __shared__ char smem[];
     const int tid = threadIdx.x, lane = lane_id(), wv = wave_id();
     const int m = blockIdx.x;
-    const int32_t N = a.N, B = a.B, RG = a.RG, LP = a.LP, D = a.D, G = a.G;
+    if (leader[m] != m) return;
+    const int32_t N = a.N, B = a.B;
     char *dst = a.dst + (int64_t)m * a.off.bytes;
     int64_t *cT = reinterpret_cast<int64_t *>(smem);  // [B]
     int64_t *cQ = cT + B;                              // [B]
@@ -572,16 +619,13 @@ __global__ void __launch_bounds__(kThreads) k_anneal_build(AnnealArgs a, const i
     int32_t *off = cN + B;                              // [B]
     int32_t *chunk = off + B;                           // [256]
     int32_t *flag = chunk + kThreads;                   // [1]
-    int64_t *red = reinterpret_cast<int64_t *>(((uintptr_t)(flag + 1) + 7) & ~(uintptr_t)7);  // [8]
+    int64_t *red = reinterpret_cast<int64_t *>(((uintptr_t)(flag + 1) + 7) & ~(uintptr_t)7);  // [4]
     const int32_t *lay = layouts + (int64_t)m * N;
     int32_t *cell_of = at<int32_t>(dst, a.off.cell);
     int32_t *pool = at<int32_t>(dst, a.off.pool);
     int32_t *start = at<int32_t>(dst, a.off.start);
     int64_t *T = at<int64_t>(dst, a.off.T);
     int64_t *Q = at<int64_t>(dst, a.off.Q);
-    int32_t *W = at<int32_t>(dst, a.off.W);
-    int64_t *Jg = at<int64_t>(dst, a.off.J);
-    int64_t *Ag = at<int64_t>(dst, a.off.A);
 
     for (int32_t c = tid; c < B; c += kThreads) {
         cT[c] = 0;
@@ -651,72 +695,94 @@ __global__ void __launch_bounds__(kThreads) k_anneal_build(AnnealArgs a, const i
         if (i < N && rank == tot - 1) off[c] += tot;
         __syncthreads();
     }
-    // W rows, A and J of every row-shard.
-    int64_t Ureg = 0;
-    int64_t jmax = LLONG_MIN;
-    for (int32_t h = 0; h < RG; ++h) {
-        const int32_t r = h / G, g = h % G;
-        int32_t acc[kMaxEPT];
+}
+
+// W row, A and J of row-shard h of leader m (grid: members x row-shards).
+__global__ void __launch_bounds__(kThreads) k_build_rows(AnnealArgs a, const int32_t *leader,
+                                                         const int32_t *status) {
+    __shared__ int64_t red[kThreads / kWave];
+    const int tid = threadIdx.x, lane = lane_id(), wv = wave_id();
+    const int64_t m = blockIdx.x / a.RG;
+    const int32_t h = (int32_t)(blockIdx.x % a.RG);
+    if (leader[m] != m || status[m] != 0) return;
+    const int32_t LP = a.LP, D = a.D, G = a.G;
+    char *dst = a.dst + m * a.off.bytes;
+    const int32_t *pool = at<int32_t>(dst, a.off.pool);
+    const int32_t *start = at<int32_t>(dst, a.off.start);
+    const int64_t *T = at<int64_t>(dst, a.off.T);
+    const int64_t *Q = at<int64_t>(dst, a.off.Q);
+    int32_t *W = at<int32_t>(dst, a.off.W);
+    const int32_t r = h / G, g = h % G;
+    int32_t acc[kMaxEPT];
 #pragma unroll
-        for (int x = 0; x < kMaxEPT; ++x) acc[x] = 0;
-        for (int32_t xs = 0; xs < a.count[g]; ++xs) {
-            const int32_t c = r * D + a.slots[g * D + xs];
-            for (int32_t pp = start[c]; pp < start[c + 1]; ++pp) {
-                const int32_t *qi = a.q + (int64_t)pool[pp] * LP;
+    for (int x = 0; x < kMaxEPT; ++x) acc[x] = 0;
+    for (int32_t xs = 0; xs < a.count[g]; ++xs) {
+        const int32_t c = r * D + a.slots[g * D + xs];
+        for (int32_t pp = start[c]; pp < start[c + 1]; ++pp) {
+            const int32_t *qi = a.q + (int64_t)pool[pp] * LP;
 #pragma unroll
-                for (int x = 0; x < kMaxEPT; ++x) {
-                    const int32_t e = tid + kThreads * x;
-                    if (x < a.nx && e < LP) acc[x] += qi[e];
-                }
-            }
-        }
-        int64_t esum = 0;
-#pragma unroll
-        for (int x = 0; x < kMaxEPT; ++x) {
-            if (x < a.nx) {
+            for (int x = 0; x < kMaxEPT; ++x) {
                 const int32_t e = tid + kThreads * x;
-                const int32_t v = e < LP ? acc[x] : INT32_MIN;
-                if (e < LP) W[(int64_t)h * LP + e] = v;
-                const int32_t mx = seg_max32(v, a.P);
-                if (e < LP && (lane & (a.P - 1)) == 0) esum += mx;
+                if (x < a.nx && e < LP) acc[x] += qi[e];
             }
         }
-        esum = wave_sum(esum);
-        if (lane == 0) red[4 + wv] = esum;
-        __syncthreads();
-        int64_t e = 0;
-        for (int w = 0; w < kThreads / kWave; ++w) e += red[4 + w];
-        __syncthreads();
-        // attention from cell statistics (count[g] <= 64 lanes)
-        int64_t A = 0;
-        {
-            const int32_t cnt = a.count[g];
-            const bool act = lane < cnt;
-            int64_t tv = 0, qv = 0;
-            if (act) {
-                const int32_t c = r * D + a.slots[g * D + lane];
-                tv = cT[c];
-                qv = cQ[c];
-            }
-            for (int s = 0; s < a.S; ++s) A += wave_max(act ? a.alpha[s] * tv + a.beta[s] * qv : LLONG_MIN);
-        }
-        const int64_t J = A + (e << a.F);
-        if (tid == 0) {
-            Jg[h] = J;
-            Ag[h] = A;
-        }
-        if (lane == g) Ureg += J;
-        jmax = J > jmax ? J : jmax;
     }
-    if (wv == 0) {
-        const int64_t s0 = wave_max(lane < G ? Ureg : LLONG_MIN);
-        const int64_t s1 = wave_sum(lane < G ? Ureg : 0);
-        if (lane == 0 && st == 0) {
-            int64_t *res = a.results + (int64_t)m * kRes;
-            res[0] = s0; res[1] = s1; res[2] = jmax;
-            res[3] = s0; res[4] = s1; res[5] = jmax;
-            res[6] = 0; res[7] = 0; res[8] = 1; res[9] = m;
+    int64_t esum = 0;
+#pragma unroll
+    for (int x = 0; x < kMaxEPT; ++x) {
+        if (x < a.nx) {
+            const int32_t e = tid + kThreads * x;
+            const int32_t v = e < LP ? acc[x] : INT32_MIN;
+            if (e < LP) W[(int64_t)h * LP + e] = v;
+            const int32_t mx = seg_max32(v, a.P);
+            if (e < LP && (lane & (a.P - 1)) == 0) esum += mx;
         }
+    }
+    esum = wave_sum(esum);
+    if (lane == 0) red[wv] = esum;
+    __syncthreads();
+    if (wv == 0) {
+        int64_t e = 0;
+        for (int w = 0; w < kThreads / kWave; ++w) e += red[w];
+        const int64_t A = attention_rs(a, T, Q, r, g, -1, 0, 0, -1, 0, 0);
+        if (lane == 0) {
+            at<int64_t>(dst, a.off.J)[h] = A + (e << a.F);
+            at<int64_t>(dst, a.off.A)[h] = A;
+        }
+    }
+}
+
+// Duplicates copy their leader's slab; every member's score goes to
+// results[m][0..2] (and the trajectory-best fields, for the incumbent).
+__global__ void __launch_bounds__(kThreads) k_build_final(AnnealArgs a, const int32_t *leader,
+                                                          int32_t *status) {
+    const int m = blockIdx.x, lane = lane_id();
+    const int ld = leader[m];
+    char *dst = a.dst + (int64_t)m * a.off.bytes;
+    if (ld != m) {
+        const int4 *src = reinterpret_cast<const int4 *>(a.dst + (int64_t)ld * a.off.bytes);
+        int4 *d4 = reinterpret_cast<int4 *>(dst);
+        for (int64_t x = threadIdx.x; x < a.off.bytes / 16; x += kThreads) d4[x] = src[x];
+        if (threadIdx.x == 0) status[m] = status[ld];
+    }
+    if (threadIdx.x >= kWave) return;
+    const int32_t st = ld != m ? status[ld] : status[m];
+    if (st != 0) return;
+    const char *slab = a.dst + (int64_t)ld * a.off.bytes;
+    const int64_t *J = reinterpret_cast<const int64_t *>(slab + a.off.J);
+    int64_t U = 0;
+    if (lane < a.G)
+        for (int r = 0; r < a.R; ++r) U += J[(int64_t)r * a.G + lane];
+    int64_t jmax = LLONG_MIN;
+    for (int h = lane; h < a.RG; h += kWave) jmax = J[h] > jmax ? J[h] : jmax;
+    const int64_t s0 = wave_max(lane < a.G ? U : LLONG_MIN);
+    const int64_t s1 = wave_sum(lane < a.G ? U : 0);
+    const int64_t s2 = wave_max(jmax);
+    if (lane == 0) {
+        int64_t *res = a.results + (int64_t)m * kRes;
+        res[0] = s0; res[1] = s1; res[2] = s2;
+        res[3] = s0; res[4] = s1; res[5] = s2;
+        res[6] = 0; res[7] = 0; res[8] = 1; res[9] = m;
     }
 }
 
@@ -986,14 +1052,23 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
     a.best = best; a.results = results;
     a.seed = prm->seed; a.p_guide = prm->p_guide_u32; a.rho = prm->rho_u32;
 
-    // Build member slabs from the population and validate them.
+    // Build member slabs from the population (each distinct layout once) and
+    // validate them.
     a.dst = slabA;
-    const size_t lds_build = (size_t)B64 * 24 + kThreads * 4 + 4 + 8 + 64 + 8;
+    uint64_t *hash = scr.get<uint64_t>(pop_size);
+    int32_t *leader = scr.get<int32_t>(pop_size);
+    if (scr.failed()) return ROUTEPACK_E_DEVICE;
+    const size_t lds_build = (size_t)B64 * 24 + kThreads * 4 + 4 + 8 + 32 + 8;
     if (lds_build > 160 * 1024) return ROUTEPACK_E_UNSUPPORTED;
-    RP_HIP(hipFuncSetAttribute((const void *)k_anneal_build, hipFuncAttributeMaxDynamicSharedMemorySize,
+    RP_HIP(hipFuncSetAttribute((const void *)k_build_cells, hipFuncAttributeMaxDynamicSharedMemorySize,
                                (int)lds_build));
-    hipLaunchKernelGGL(k_anneal_build, dim3(pop_size), dim3(kThreads), lds_build, stream, a,
-                       population, status);
+    hipLaunchKernelGGL(k_layout_hash, dim3(pop_size), dim3(kThreads), 0, stream, population, N, hash);
+    hipLaunchKernelGGL(k_leader, dim3(pop_size), dim3(64), 0, stream, population, N, hash, leader);
+    hipLaunchKernelGGL(k_build_cells, dim3(pop_size), dim3(kThreads), lds_build, stream, a, population,
+                       leader, status);
+    hipLaunchKernelGGL(k_build_rows, dim3((unsigned)(pop_size * RG64)), dim3(kThreads), 0, stream, a,
+                       leader, status);
+    hipLaunchKernelGGL(k_build_final, dim3(pop_size), dim3(kThreads), 0, stream, a, leader, status);
     RP_HIP(hipGetLastError());
     std::vector<int32_t> hstat(pop_size);
     RP_HIP(hipMemcpyAsync(hstat.data(), status, sizeof(int32_t) * pop_size, hipMemcpyDeviceToHost, stream));
@@ -1052,6 +1127,15 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_level));
     char *src = slabA, *dst = slabB;
     const int32_t *cur_parent = nullptr;
+    std::vector<hipEvent_t> ev;
+    if (prm->level_kernel_ms) {
+        ev.resize(2 * (size_t)prm->n_sweeps);
+        for (auto &e : ev) RP_HIP(hipEventCreate(&e));
+    }
+    struct EventGuard {
+        std::vector<hipEvent_t> &v;
+        ~EventGuard() { for (auto e : v) (void)hipEventDestroy(e); }
+    } ev_guard{ev};
     for (int n = 0; n < prm->n_sweeps; ++n) {
         a.src = src;
         a.dst = dst;
@@ -1059,10 +1143,12 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
         a.level = prm->sweep_offset + n;
         a.temp = prm->temperatures[n];
         a.step_log = step_log ? step_log + (size_t)n * pop_size * a.K : nullptr;
+        if (!ev.empty()) RP_HIP(hipEventRecord(ev[2 * n], stream));
         if (wlds)
             hipLaunchKernelGGL(k_anneal_level<true>, dim3(pop_size), dim3(kThreads), lds_level, stream, a);
         else
             hipLaunchKernelGGL(k_anneal_level<false>, dim3(pop_size), dim3(kThreads), lds_level, stream, a);
+        if (!ev.empty()) RP_HIP(hipEventRecord(ev[2 * n + 1], stream));
         const double t_after = (n + 1 < prm->n_sweeps) ? prm->temperatures[n + 1] : prm->t_next;
         le.src_slabs = src;
         le.trace = trace ? trace + (size_t)n * pop_size * 8 : nullptr;
@@ -1089,6 +1175,11 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
     RP_HIP(hipMemcpyAsync(&ok, chk, sizeof(ok), hipMemcpyDeviceToHost, stream));
     RP_HIP(hipMemcpyAsync(hx, best_score, sizeof(hx), hipMemcpyDeviceToHost, stream));
     RP_HIP(hipStreamSynchronize(stream));
+    for (int n = 0; n < (int)ev.size() / 2; ++n) {
+        float ms = 0.0f;
+        RP_HIP(hipEventElapsedTime(&ms, ev[2 * n], ev[2 * n + 1]));
+        prm->level_kernel_ms[n] = ms;
+    }
     if (!ok) return ROUTEPACK_E_INTERNAL;
     if (lex_less(ref[0], ref[1], ref[2], hx[0], hx[1], hx[2])) return ROUTEPACK_E_INTERNAL;
     return ROUTEPACK_OK;

@@ -78,31 +78,41 @@ __global__ void k_length_stats(const int32_t *__restrict__ t, int64_t n, int64_t
     }
 }
 
-// tot[l] += sum_p q[i][l][p]; neg set when any q < 0.
-__global__ void k_layer_totals(const int32_t *__restrict__ q, int64_t rows, int32_t L, int32_t P,
-                               unsigned long long *tot, int32_t *neg) {
+// tot[l] += sum_p q[i][l][p]; rate = max over rows of ceil(max_p q / t_i);
+// neg set when any q < 0.
+__global__ void k_layer_totals(const int32_t *__restrict__ q, const int32_t *__restrict__ t,
+                               int64_t rows, int32_t L, int32_t P, unsigned long long *tot,
+                               long long *rate, int32_t *neg) {
+    long long rmax = 0;
     for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < rows;
          r += (int64_t)gridDim.x * blockDim.x) {
         const int32_t *row = q + r * P;
-        int64_t s = 0;
+        int64_t s = 0, mx = 0;
         int bad = 0;
         for (int p = 0; p < P; ++p) {
             const int32_t v = row[p];
             s += v;
+            mx = v > mx ? v : mx;
             bad |= (v < 0);
         }
+        const int64_t ti = t[r / L];
+        const long long rt = ti > 0 ? (mx + ti - 1) / ti : mx;
+        rmax = rt > rmax ? rt : rmax;
         if (s) atomicAdd(&tot[r % L], (unsigned long long)s);
         if (bad) atomicOr(neg, 1);
     }
+    rmax = wave_max(rmax);
+    if (lane_id() == 0) atomicMax(rate, rmax);
 }
 
-__global__ void k_init_stats(unsigned long long *u, long long *mx, long long *mn, int32_t *neg,
-                             int32_t L) {
+__global__ void k_init_stats(unsigned long long *u, long long *mx, long long *mn, long long *rate,
+                             int32_t *neg, int32_t L) {
     const int i = threadIdx.x;
     if (i < 2) u[i] = 0;
     if (i == 0) {
         *mx = LLONG_MIN;
         *mn = LLONG_MAX;
+        *rate = 0;
         *neg = 0;
     }
     for (int l = i; l < L; l += blockDim.x) u[2 + l] = 0;
@@ -114,10 +124,10 @@ int window_stats(const routepack_problem *p, const int32_t *lengths, const int32
     Scratch scr(stream);
     // layout: u[0] sum, u[1] big, u[2..2+L) layer totals; then mx, mn, neg
     unsigned long long *u = scr.get<unsigned long long>(2 + L);
-    long long *mm = scr.get<long long>(2);
+    long long *mm = scr.get<long long>(3);
     int32_t *neg = scr.get<int32_t>(1);
     if (scr.failed()) return ROUTEPACK_E_DEVICE;
-    hipLaunchKernelGGL(k_init_stats, dim3(1), dim3(256), 0, stream, u, mm, mm + 1, neg, L);
+    hipLaunchKernelGGL(k_init_stats, dim3(1), dim3(256), 0, stream, u, mm, mm + 1, mm + 2, neg, L);
     const int64_t n = p->n_samples;
     int blocks = (int)((n + 255) / 256);
     if (blocks > 1024) blocks = 1024;
@@ -127,12 +137,12 @@ int window_stats(const routepack_problem *p, const int32_t *lengths, const int32
         const int64_t rows = n * L;
         int qb = (int)((rows + 255) / 256);
         if (qb > 4096) qb = 4096;
-        hipLaunchKernelGGL(k_layer_totals, dim3(qb), dim3(256), 0, stream, q, rows, L,
-                           p->n_ranks, u + 2, neg);
+        hipLaunchKernelGGL(k_layer_totals, dim3(qb), dim3(256), 0, stream, q, lengths, rows, L,
+                           p->n_ranks, u + 2, mm + 2, neg);
     }
     RP_HIP(hipGetLastError());
     std::vector<unsigned long long> hu(2 + L);
-    long long hm[2];
+    long long hm[3];
     int32_t hneg = 0;
     RP_HIP(hipMemcpyAsync(hu.data(), u, sizeof(unsigned long long) * (2 + L),
                           hipMemcpyDeviceToHost, stream));
@@ -147,6 +157,7 @@ int window_stats(const routepack_problem *p, const int32_t *lengths, const int32
     for (int l = 0; l < L; ++l)
         if ((int64_t)hu[2 + l] > out->w_bound) out->w_bound = (int64_t)hu[2 + l];
     out->q_negative = hneg != 0;
+    out->q_rate = hm[2];
     return ROUTEPACK_OK;
 }
 
@@ -154,14 +165,24 @@ int overflow_check(const routepack_problem *p, int64_t n_rows, const WindowStats
                    bool w_as_int32) {
     const long double lim = 9007199254740992.0L;  // 2^53
     const long double C = (long double)p->capacity;
+    // W bound of a capacity-feasible layout: a row-shard holds at most
+    // maxD * C tokens and q[i][l][p] <= rate * t_i.
+    int32_t maxd = 0;
+    {
+        std::vector<int32_t> cnt(p->n_edp, 0);
+        for (int d = 0; d < p->n_dp; ++d) cnt[p->dp_to_edp[d]]++;
+        for (int g = 0; g < p->n_edp; ++g) maxd = cnt[g] > maxd ? cnt[g] : maxd;
+    }
+    const long double wcap = (long double)ws.q_rate * (long double)maxd * C;
+    const int64_t wb = wcap < (long double)ws.w_bound ? (int64_t)wcap : ws.w_bound;
     long double a_max = 0.0L;
     for (int s = 0; s < p->n_stages; ++s)
         a_max += (long double)p->alpha_fp[s] * C + (long double)p->beta_fp[s] * C * C;
-    const long double e_max = ldexpl((long double)p->n_layers * (long double)ws.w_bound, p->frac_bits);
+    const long double e_max = ldexpl((long double)p->n_layers * (long double)wb, p->frac_bits);
     const long double total = (long double)n_rows * (long double)p->n_edp * (a_max + e_max + 1.0L);
     if (!(total < lim)) return ROUTEPACK_E_OVERFLOW;
     if (!(ldexpl(C, p->frac_bits) < lim)) return ROUTEPACK_E_OVERFLOW;
-    if (w_as_int32 && ws.w_bound > 2147483647LL) return ROUTEPACK_E_OVERFLOW;
+    if (w_as_int32 && wb > 2147483647LL) return ROUTEPACK_E_OVERFLOW;
     return ROUTEPACK_OK;
 }
 

@@ -56,13 +56,16 @@ class Scratch {
 struct WindowStats {
     int64_t sum_t = 0, max_t = 0, min_t = 0, n_big = 0;  // n_big: t_i > C/2
     int64_t w_bound = 0;                                  // max_l sum_{i,p} q[i][l][p]
+    int64_t q_rate = 0;                                   // max_i ceil(max_{l,p} q[i][l][p] / t_i)
     bool q_negative = false;
 };
 int window_stats(const routepack_problem *p, const int32_t *lengths, const int32_t *q,
                  WindowStats *out, hipStream_t stream);
 
 // R * G * (A_max + E_max + 1) < 2^53 and 2^F * C < 2^53 (scores exact in
-// int64 and as doubles); also W entries must fit int32 when as_int32.
+// int64 and as doubles), with W bounded by min(w_bound, q_rate * maxD * C)
+// for capacity-feasible layouts; W entries must also fit int32 when
+// w_as_int32.
 int overflow_check(const routepack_problem *p, int64_t n_rows, const WindowStats &ws,
                    bool w_as_int32);
 

@@ -33,6 +33,7 @@ int eval_layouts(const routepack_problem *p, const Topology &topo, const DeviceP
                  const int32_t *t, const int32_t *q, int32_t R, int64_t n, const int32_t *layouts,
                  int64_t *scores, int32_t *status, int64_t *J, double *diag,
                  const int64_t *rank_load, hipStream_t stream);
+__global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v);
 
 constexpr int kMaxCells = 4096;
 
@@ -198,10 +199,12 @@ __global__ void __launch_bounds__(64) k_pack_trials(TrialArgs a) {
             } else {
                 // RandomizedBestFit: rank the feasible cells and take the
                 // rho-th of the leading min(w, |F|).
+                // (uniform trip count: every lane takes part in each ballot)
                 int32_t nf = 0;
                 int64_t bT = -1; int32_t bn = 0, bc = -1;
-                for (int32_t cc = lane; cc < K; cc += kWave) {
-                    const bool f = sT[cc] + ti <= a.C;
+                for (int32_t cb = 0; cb < K; cb += kWave) {
+                    const int32_t cc = cb + lane;
+                    const bool f = cc < K && sT[cc] + ti <= a.C;
                     if (f && (bc < 0 || fit_before(sT[cc], sN[cc], cc, bT, bn, bc))) {
                         bT = sT[cc]; bn = sN[cc]; bc = cc;
                     }
@@ -288,8 +291,9 @@ __global__ void __launch_bounds__(64) k_pack_trials(TrialArgs a) {
         const int32_t k = order[pos];
         const int32_t *Qk = Qc + (int64_t)k * LP;
         int32_t cnt = 0;
-        for (int32_t h = lane; h < RG; h += kWave) {
-            const bool cand = filled[h] < a.count[h % G];
+        for (int32_t hb = 0; hb < RG; hb += kWave) {
+            const int32_t h = hb + lane;
+            const bool cand = h < RG && filled[h] < a.count[h % G];
             int64_t af = 0, pk = 0;
             if (cand) {
                 const int32_t *Wh = Wt + (int64_t)h * LP;
@@ -300,8 +304,10 @@ __global__ void __launch_bounds__(64) k_pack_trials(TrialArgs a) {
                     pk = mx > pk ? mx : pk;
                 }
             }
-            after[h] = af;
-            pkv[h] = pk;
+            if (h < RG) {
+                after[h] = af;
+                pkv[h] = pk;
+            }
             cnt += __popcll(__ballot(cand));
         }
         __syncthreads();
@@ -371,7 +377,10 @@ __global__ void __launch_bounds__(256) k_canonical(const int32_t *layouts, int32
     int32_t *rkey = rowkey_g + (int64_t)b * R;
     for (int32_t c = tid; c < B; c += blockDim.x) cmin[c] = INT32_MAX;
     __syncthreads();
-    for (int32_t i = tid; i < N; i += blockDim.x) atomicMin(&cmin[lay[i]], i);
+    for (int32_t i = tid; i < N; i += blockDim.x) {
+        const int32_t c = lay[i];
+        if (c >= 0 && c < B) atomicMin(&cmin[c], i);
+    }
     __syncthreads();
     // slot of each cell within its row-shard after ordering by smallest id
     for (int32_t c = tid; c < B; c += blockDim.x) {
@@ -386,6 +395,8 @@ __global__ void __launch_bounds__(256) k_canonical(const int32_t *layouts, int32
     }
     __syncthreads();
     // row key: smallest id of the cell that lands in slot 0
+    for (int32_t r = tid; r < R; r += blockDim.x) rkey[r] = INT32_MAX;
+    __syncthreads();
     for (int32_t c = tid; c < B; c += blockDim.x)
         if (newd[c] == 0) rkey[c / D] = cmin[c];
     __syncthreads();
@@ -397,13 +408,17 @@ __global__ void __launch_bounds__(256) k_canonical(const int32_t *layouts, int32
         newd[c] = rank * D + newd[c];
     }
     __syncthreads();
-    for (int32_t i = tid; i < N; i += blockDim.x) canon[(int64_t)b * N + i] = newd[lay[i]];
+    for (int32_t i = tid; i < N; i += blockDim.x) {
+        const int32_t c = lay[i];
+        canon[(int64_t)b * N + i] = (c >= 0 && c < B) ? newd[c] : -1;
+    }
 }
 
 // Selection and cyclic fill.  cand m: 0 x_length, 1 x_paired (kept when
 // strictly better than x_length), m >= 2 trial m-1 (kept when it succeeded).
 __global__ void __launch_bounds__(256) k_pack_select(const int32_t *canon, const int64_t *scores,
-                                                     const int32_t *ok, int32_t M, int32_t N,
+                                                     const int32_t *ok, const int32_t *status,
+                                                     int32_t M, int32_t N,
                                                      int32_t *keep_order, int32_t *meta) {
     __shared__ int32_t valid[64], kept[64], order[64];
     __shared__ int32_t differ;
@@ -412,9 +427,9 @@ __global__ void __launch_bounds__(256) k_pack_select(const int32_t *canon, const
         int32_t v = 1;
         if (tid == 1) {
             const int64_t *a = scores + 3, *x = scores;
-            v = ok[0] && lex_less(a[0], a[1], a[2], x[0], x[1], x[2]);
+            v = ok[0] && status[1] == 0 && lex_less(a[0], a[1], a[2], x[0], x[1], x[2]);
         } else if (tid >= 2) {
-            v = ok[tid - 1];
+            v = ok[tid - 1] && status[tid] == 0;
         }
         valid[tid] = v;
         kept[tid] = 0;
@@ -457,7 +472,7 @@ __global__ void __launch_bounds__(256) k_pack_select(const int32_t *canon, const
         }
         for (int x = 0; x < n; ++x) keep_order[x] = order[x];
         int32_t ntr = 0;
-        for (int m = 2; m < M; ++m) ntr += ok[m - 1];
+        for (int m = 2; m < M; ++m) ntr += ok[m - 1] && status[m] == 0;
         meta[0] = n;
         meta[1] = ntr;
     }
@@ -561,17 +576,21 @@ extern "C" int routepack_pack_rows(const routepack_problem *prob, const int32_t 
     ta.ok = okv;
     if (M > 2)
         hipLaunchKernelGGL(k_seed_words, dim3(1024), dim3(256), 0, stream, seed, M, N, K, words);
+    // every candidate slot starts as a valid layout (all samples in cell 0),
+    // so a failed trial never leaves indices outside [0, R*D)
+    hipLaunchKernelGGL(k_fill_i32, dim3(256), dim3(256), 0, stream, cand, (int64_t)M * N, 0);
+    hipLaunchKernelGGL(k_fill_i32, dim3(1), dim3(64), 0, stream, okv, (int64_t)M, 0);
     RP_HIP(hipMemcpyAsync(cand, x_len, sizeof(int32_t) * N, hipMemcpyDeviceToDevice, stream));
     hipLaunchKernelGGL(k_pack_trials, dim3(nb), dim3(64), 0, stream, ta);
     RP_HIP(hipGetLastError());
     // Score every candidate (failed trials leave garbage layouts: their
     // status is nonzero or they are ignored by the selection).
-    hipLaunchKernelGGL(k_fill_i32_pack, dim3(1), dim3(64), 0, stream, cand, 0, 0);
     RP_TRY(eval_layouts(prob, topo, dp, lengths, q, (int32_t)R, M, cand, cscore, cstat, nullptr,
                         nullptr, nullptr, stream));
     hipLaunchKernelGGL(k_canonical, dim3(M), dim3(256), 0, stream, cand, M, N, (int32_t)R, D, G,
                        dp.slots, dp.count, dp.slot_shard, cmin, newc, rkey, canon);
-    hipLaunchKernelGGL(k_pack_select, dim3(1), dim3(256), 0, stream, canon, cscore, okv, M, N, keep, meta);
+    hipLaunchKernelGGL(k_pack_select, dim3(1), dim3(256), 0, stream, canon, cscore, okv, cstat, M, N, keep,
+                       meta);
     hipLaunchKernelGGL(k_pack_fill, dim3(pop_size), dim3(256), 0, stream, canon, cscore, keep, meta, N,
                        population, scores);
     RP_HIP(hipGetLastError());

@@ -148,10 +148,11 @@ def _capped_multinomial(rng, totals, p, cap):
     return counts
 
 
-def _demand(rng, cfg, t):
-    n, L, E, k = cfg["n"], cfg["layers"], cfg["experts"], cfg["top_k"]
+def _layer_profiles(rng, cfg):
+    """Per-layer Zipf profiles p_l over the experts (structural stream)."""
+    L, E = cfg["layers"], cfg["experts"]
     s, mode = cfg["zipf"], cfg["mode"]
-    out = np.empty((n, L, E), dtype=np.int32)
+    profiles = np.empty((L, E), dtype=np.float64)
     perm = rng.permutation(E)
     for l in range(L):
         if mode in ("perm", "dirichlet", "hot"):
@@ -164,14 +165,38 @@ def _demand(rng, cfg, t):
         if mode == "hot":
             hot = rng.choice(E, size=5, replace=False)
             p[hot] *= 4.0
-        p = p / p.sum()
-        if mode == "dirichlet":
-            pp = rng.dirichlet(50.0 * p, size=n)
-            pp = np.maximum(pp, 0.0)
-            pp = pp / pp.sum(axis=1, keepdims=True)
-        else:
-            pp = p
-        out[:, l, :] = _capped_multinomial(rng, k * t, pp, t)
+        profiles[l] = p / p.sum()
+    return profiles
+
+
+def _layer_demand(args):
+    """Counts of one layer from its own stream: [2608, 12146, index, 1 + l]."""
+    index, l, p, mode, k, t = args
+    rng = np.random.default_rng([2608, 12146, index, 1 + l])
+    if mode == "dirichlet":
+        pp = rng.dirichlet(50.0 * p, size=t.shape[0])
+        pp = np.maximum(pp, 0.0)
+        pp = pp / pp.sum(axis=1, keepdims=True)
+    else:
+        pp = p
+    return _capped_multinomial(rng, k * t, pp, t).astype(np.int32)
+
+
+def _demand(rng, cfg, t, workers=None):
+    n, L, E, k = cfg["n"], cfg["layers"], cfg["experts"], cfg["top_k"]
+    profiles = _layer_profiles(rng, cfg)
+    out = np.empty((n, L, E), dtype=np.int32)
+    jobs = [(cfg["index"], l, profiles[l], cfg["mode"], k, t) for l in range(L)]
+    if workers is None:
+        workers = min(16, os.cpu_count() or 1) if n * L * E >= (1 << 22) else 1
+    if workers > 1:
+        import multiprocessing as mp
+        with mp.get_context("fork").Pool(workers) as pool:
+            for l, counts in enumerate(pool.imap(_layer_demand, jobs)):
+                out[:, l, :] = counts
+    else:
+        for l, job in enumerate(jobs):
+            out[:, l, :] = _layer_demand(job)
     return out
 
 

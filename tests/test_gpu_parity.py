@@ -178,6 +178,70 @@ def test_anneal_mid_sampled_levels():
 
 
 @gpu
+@pytest.mark.parametrize("name,G", [("tiny", 1), ("tiny", 2), ("small", 1), ("small", 4),
+                                    ("mid", 1), ("mid", 2)])
+def test_pack_rows(name, G):
+    rp = _rp()
+    _log(f"pack_rows {name} G={G}")
+    w, pd, pb, agg, slot, load, q = _window(name, G)
+    pr = _packed(name, G)
+    g = rp.pack_rows(rp.Problem.from_dict(pd), w.lengths, q, w.seed_pack, synth.windows.N_TRIALS,
+                     synth.windows.CHOICE_WIDTH, w.pop)
+    assert (g["r_star"], g["certified"]) == (pr["r_star"], pr["certified"])
+    assert (g["r_lb"], g["n_distinct"], g["n_trials_ok"]) == (pr["r_lb"], pr["n_distinct"], pr["n_trials_ok"])
+    assert np.array_equal(g["population"].cpu().numpy(), pr["population"])
+    assert np.array_equal(g["scores"].cpu().numpy(), pr["scores"])
+
+
+@gpu
+@pytest.mark.parametrize("seed", range(6))
+def test_pack_rows_random_tiny(seed):
+    """Random tiny windows, including widths above the cell count and
+    topologies with several shards."""
+    import oracle as O
+    rp = _rp()
+    rng = np.random.default_rng([5, seed])
+    D = int(rng.choice([1, 2, 4]))
+    G = int(rng.choice([g for g in (1, 2, 4) if g <= D and D % g == 0]))
+    n = int(rng.integers(3 * D, 12 * D))
+    w = synth.make_tiny_random(100 + seed, n=n, layers=int(rng.integers(0, 4)), experts=8, ranks=4,
+                               dp=D, edp=G, cap=200, tmin=5, tmax=120)
+    pd = synth.window_problem(w)
+    pb = O.Problem.from_dict(pd)
+    slot, _ = O.place(O.aggregate(w.demand), w.n_ranks)
+    q = O.project(w.demand, slot, w.n_ranks)
+    width = int(rng.integers(1, 9))
+    o = O.pack_rows(pb, w.lengths, q, seed, 8, width, 5)
+    if o["rc"] != 0:
+        with pytest.raises(rp.RoutepackError) as ei:
+            rp.pack_rows(rp.Problem.from_dict(pd), w.lengths, q, seed, 8, width, 5)
+        assert ei.value.code == o["rc"]
+        return
+    g = rp.pack_rows(rp.Problem.from_dict(pd), w.lengths, q, seed, 8, width, 5)
+    assert (g["r_star"], g["certified"], g["n_distinct"], g["n_trials_ok"]) == \
+        (o["r_star"], o["certified"], o["n_distinct"], o["n_trials_ok"])
+    assert np.array_equal(g["population"].cpu().numpy(), o["population"])
+    assert np.array_equal(g["scores"].cpu().numpy(), o["scores"])
+
+
+@gpu
+def test_pack_rows_errors():
+    rp = _rp()
+    prob = rp.Problem(4, 1, 2, 1, 2, 2, 1, [0, 0], 10, [4096], [0])
+    q = np.zeros((4, 1, 2), dtype=np.int32)
+    with pytest.raises(rp.RoutepackError) as ei:          # a sample longer than C
+        rp.pack_rows(prob, [11, 1, 1, 1], q, 1, 4, 2, 2)
+    assert ei.value.code == -2
+    prob3 = rp.Problem(3, 1, 2, 1, 2, 2, 1, [0, 0], 10, [4096], [0])
+    with pytest.raises(rp.RoutepackError) as ei:          # floor(N/D) below the bound
+        rp.pack_rows(prob3, [9, 9, 9], np.zeros((3, 1, 2), np.int32), 1, 4, 2, 2)
+    assert ei.value.code == -2
+    with pytest.raises(rp.RoutepackError) as ei:          # width out of range
+        rp.pack_rows(prob, [1, 1, 1, 1], q, 1, 4, 0, 2)
+    assert ei.value.code == -1
+
+
+@gpu
 def test_anneal_resume_is_exact_on_gpu():
     rp = _rp()
     w, pd, pb, agg, slot, load, q = _window("tiny")
