@@ -1,0 +1,227 @@
+#!/usr/bin/env python3
+"""Benchmark of the RoutePack planner hot path on one MI355X.
+
+One step is one pass of the whole path over one synthetic optimizer-step
+window already resident in HBM: demand aggregation, LPT placement and rank
+projection, row packing with the seed population, and population annealing
+over the full temperature schedule (plus the library's own validation of x*).
+
+Workload (default): the mid window -- 4096 samples with lognormal lengths
+(median 4096, sigma 1.0, clipped to [128, 32768]), 24 MoE layers of 256
+experts, top-8 routing with a Zipf(1.2) profile drifting 10% per layer,
+16 EP ranks, 8 DP slots in one EDP shard, cap 65536 tokens; population 1024,
+2000 levels of 256 proposals.
+
+Metric: annealing move-evals/s = evaluated (feasible) proposals of all
+levels and members, over the wall time of the steps.  The JSON line also
+carries the roofline of the dominant kernel (k_anneal_level) from HIP events
+on the library's stream, and the CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+PMC_FILE = os.path.join(ROOT, "profiles", "anneal_level_mid_pmc.txt")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_12146_amd", "csrc", f)
+                  for f in ("rp_anneal.hip", "rp_device.h")]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def read_pmc():
+    """Counter-derived HBM traffic per dispatch, if taken on this kernel source."""
+    if not os.path.exists(PMC_FILE):
+        return None
+    kv = {}
+    for line in open(PMC_FILE):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    try:
+        return float(kv["hbm_bytes_per_dispatch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def workload_text(w, G):
+    return (f"{w.name} window: {w.n} samples, {w.n_layers} layers x {w.n_experts} experts top-{w.top_k}, "
+            f"{w.n_ranks} EP ranks, {w.n_dp} DP slots in {G} EDP shard(s), cap {w.capacity}, "
+            f"population {w.pop}, {w.levels} levels x 256 proposals")
+
+
+def copy_probe():
+    """A plain copy of known size, for scaling FETCH_SIZE / WRITE_SIZE."""
+    import torch
+    n = 256 << 20
+    src = torch.ones(n // 4, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": n, "dispatches": 5}))
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--window", default="mid")
+    ap.add_argument("--edp", type=int, default=1, help="EDP shards G (contiguous slot blocks)")
+    ap.add_argument("--levels", type=int, default=None, help="levels (default: the window's schedule)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-levels", type=int, default=16, help="levels in the oracle's timed sample")
+    ap.add_argument("--copy-probe", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the planner path is "
+              "single-GPU and multi-GPU sharding is not part of this build", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    if args.copy_probe:
+        copy_probe()
+        return
+
+    import paper_2608_12146_amd as rp
+    import synth
+    from synth import windows as W
+
+    w = synth.make_window(args.window, edp=args.edp)
+    pd = synth.window_problem(w)
+    prob = rp.Problem.from_dict(pd)
+    levels = args.levels or w.levels
+    temps = synth.anneal_temperatures(w.levels)[:levels]
+    K = W.STEPS_PER_LEVEL
+    demand = torch.as_tensor(w.demand, device="cuda")
+    lengths = torch.as_tensor(w.lengths, device="cuda")
+    torch.cuda.synchronize()
+
+    def step():
+        agg = rp.aggregate_demand(prob, demand)
+        slot, load, q = rp.place_experts(prob, agg, demand)
+        pk = rp.pack_rows(prob, lengths, q, w.seed_pack, W.N_TRIALS, W.CHOICE_WIDTH, w.pop)
+        an = rp.anneal(prob, lengths, q, pk["r_star"], pk["population"], temps, K, w.seed_anneal,
+                       want_parents=False, kernel_times=True)
+        return q, load, pk, an
+
+    def progress(msg):
+        print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+    progress(f"{workload_text(w, args.edp)}; levels {levels}")
+    for k in range(args.warmup):
+        t1 = time.perf_counter()
+        step()
+        torch.cuda.synchronize()
+        progress(f"warmup {k} {time.perf_counter() - t1:.2f} s")
+    evals = acc = 0
+    kernel_ms = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        q, load, pk, an = step()
+        tr = an["trace"]
+        evals += int(tr[:, :, 7].sum().item())
+        acc += int(tr[:, :, 6].sum().item())
+        kernel_ms.append(an["level_kernel_ms"])
+        progress(f"step done at {time.perf_counter() - t0:.2f} s")
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    attempted = args.steps * levels * w.pop * K
+
+    # Roofline of k_anneal_level: algorithmic global bytes of an evaluated
+    # move are the moved samples' q rows (2 L P int32 for a swap, L P for a
+    # relocation), expected (2 - rho) L P 4 bytes at relocation rate rho.
+    rho = W.RHO_U32 / 2.0**32
+    bytes_per_eval = (2.0 - rho) * w.n_layers * w.n_ranks * 4
+    kms = np.concatenate(kernel_ms)
+    k_sec = float(kms.sum()) / 1e3
+    achieved = evals * bytes_per_eval / k_sec / 1e9
+    traffic = read_pmc()
+
+    # Objective == oracle: the oracle rescoring of the GPU's x*, the oracle's
+    # seed population, and one level of three members recomputed by the oracle.
+    import oracle as O
+    pb = O.Problem.from_dict(pd)
+    qn = q.cpu().numpy()
+    st, s_or, _, _ = O.score(pb, w.lengths, qn, pk["r_star"], an["best_layout"].cpu().numpy())
+    score_ok = st == 0 and s_or.tolist() == an["best_score"].cpu().tolist()
+    opk = O.pack_rows(pb, w.lengths, qn, w.seed_pack, W.N_TRIALS, W.CHOICE_WIDTH, w.pop)
+    pack_ok = (opk["r_star"] == pk["r_star"]
+               and bool(np.array_equal(opk["population"], pk["population"].cpu().numpy()))
+               and bool(np.array_equal(opk["scores"], pk["scores"].cpu().numpy())))
+    ids = np.array([0, 1, w.pop - 1], dtype=np.int32)
+    g1 = rp.anneal(prob, lengths, q, pk["r_star"], torch.as_tensor(opk["population"], device="cuda"),
+                   temps[:1], K, w.seed_anneal, want_parents=False)
+    o1 = O.anneal(pb, w.lengths, qn, opk["r_star"], opk["population"][ids], temps[:1], K, w.seed_anneal,
+                  replica_ids=ids, want_parents=False)
+    level_ok = bool(np.array_equal(g1["trace"].cpu().numpy()[0][ids], o1["trace"][0]))
+
+    progress(f"parity: x* {score_ok}, pack {pack_ok}, level {level_ok}")
+    cpu = None
+    if not args.no_cpu_baseline:
+        progress("cpu baseline (oracle)")
+        threads = min(16, os.cpu_count() or 1)
+        nl = min(args.cpu_levels, levels)
+        tc = time.perf_counter()
+        oc = O.anneal(pb, w.lengths, qn, opk["r_star"], opk["population"], temps[:nl], K, w.seed_anneal,
+                      t_next=(temps[nl] if nl < len(temps) else 0.0), n_threads=threads,
+                      want_parents=False)
+        tcpu = time.perf_counter() - tc
+        cev = int(oc["trace"][:, :, 7].sum())
+        cpu = {"value": cev / tcpu, "unit": "move-evals/s", "cores": threads, "kind": "oracle",
+               "sample": f"levels 0-{nl - 1} of the same schedule, population {w.pop}, "
+                         f"{cev} evaluated moves in {tcpu:.1f} s on {threads} threads"}
+
+    out = {
+        "metric": "anneal move-evals/sec; objective==oracle; % HBM/LDS roofline",
+        "value": evals / dt,
+        "unit": "move-evals/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": dt / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {"workload": workload_text(w, args.edp), "levels": levels, "proposals_per_level": K},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "kernel": "k_anneal_level", "avg_launch_ms": float(kms.mean()),
+                     "bytes_per_eval": bytes_per_eval},
+        "cpu_baseline": cpu,
+        "attempted_per_s": attempted / dt,
+        "evals_per_step": evals // args.steps,
+        "accept_rate": acc / max(evals, 1),
+        "parity": {"x_star_score_eq_oracle": bool(score_ok), "pack_eq_oracle": bool(pack_ok),
+                   "level0_sampled_members_eq_oracle": level_ok},
+        "r_star": pk["r_star"],
+        "best_score": an["best_score"].cpu().tolist(),
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
