@@ -94,7 +94,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the planner path is "
-              "single-GPU and multi-GPU sharding is not part of this build", file=sys.stderr)
+              "single-GPU; sharding the population across GPUs is not implemented", file=sys.stderr)
         sys.exit(2)
     import torch
     if not torch.cuda.is_available():

@@ -49,7 +49,7 @@ extern "C" {
 #define ROUTEPACK_E_OVERFLOW    -5  /* R*G*(A_max + E_max + 1) >= 2^53: scores not exact in int64/double */
 #define ROUTEPACK_E_DEVICE      -6  /* a HIP runtime error */
 #define ROUTEPACK_E_INTERNAL    -7  /* a postcondition failed (validation of x*, non-regression) */
-#define ROUTEPACK_E_UNSUPPORTED -8  /* a size this build's kernels do not handle (documented per call) */
+#define ROUTEPACK_E_UNSUPPORTED -8  /* a size these kernels do not handle (documented per call) */
 
 /* Problem description (Sec. 3.1-3.4).
  * demand a[i][l][e] and lengths t_i are the routing-replay input (Eq.
