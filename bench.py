@@ -149,7 +149,7 @@ def main():
     dt = time.perf_counter() - t0
     attempted = args.steps * levels * w.pop * K
 
-    # Roofline of k_anneal_level: algorithmic global bytes of an evaluated
+    # Roofline of the level kernel (k_anneal_wave): algorithmic global bytes of an evaluated
     # move are the moved samples' q rows (2 L P int32 for a swap, L P for a
     # relocation), expected (2 - rho) L P 4 bytes at relocation rate rho.
     rho = W.RHO_U32 / 2.0**32
@@ -209,7 +209,7 @@ def main():
         "config": {"workload": workload_text(w, args.edp), "levels": levels, "proposals_per_level": K},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "k_anneal_level", "avg_launch_ms": float(kms.mean()),
+                     "kernel": "k_anneal_wave", "avg_launch_ms": float(kms.mean()),
                      "bytes_per_eval": bytes_per_eval},
         "cpu_baseline": cpu,
         "attempted_per_s": attempted / dt,

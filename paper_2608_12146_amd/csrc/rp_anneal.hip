@@ -21,11 +21,13 @@
 // barriers are the cross-wave sum of the two E' partials of a feasible
 // proposal and the commit of an accepted one.
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
 #include <vector>
 
+#include "rp_anneal.h"
 #include "rp_device.h"
 #include "rp_internal.h"
 
@@ -36,160 +38,6 @@ int eval_layouts(const routepack_problem *p, const Topology &topo, const DeviceP
                  int64_t *scores, int32_t *status, int64_t *J, double *diag,
                  const int64_t *rank_load, hipStream_t stream);
 __global__ void k_fill_i32(int32_t *p, int64_t n, int32_t v);
-
-constexpr int kThreads = 256;
-constexpr int kMaxEPT = 16;   // W entries per thread: L*P <= 4096
-constexpr int kMaxJPL = 8;    // row-shards per lane: R*G <= 512
-constexpr int kMaxStages = 4;
-constexpr int kRes = 10;      // per-member result words
-
-struct SlabOffsets {
-    int64_t cell, pool, start, T, Q, W, J, A, bytes;
-};
-
-struct AnnealArgs {
-    const int32_t *t, *q;
-    int32_t N, L, P, D, G, R, S, F, K;
-    int32_t LP, RG, B, nx, pshift;
-    int64_t C;
-    double scale, temp;
-    int64_t alpha[kMaxStages], beta[kMaxStages];
-    const int32_t *slots, *count, *slot_shard;
-    char *src, *dst;
-    SlabOffsets off;
-    const int32_t *parent;  // [pop] or null (identity)
-    int32_t *best;          // [pop][N]
-    int64_t *results;       // [pop][kRes]
-    uint8_t *step_log;      // [pop][K] or null
-    uint64_t seed;
-    int32_t level;
-    uint32_t p_guide, rho;
-};
-
-template <class T>
-__device__ __host__ inline T *at(char *base, int64_t off) {
-    return reinterpret_cast<T *>(base + off);
-}
-
-__device__ inline uint64_t readlane64(uint64_t v, int lane) {
-    const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)v, lane);
-    const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), lane);
-    return ((uint64_t)hi << 32) | lo;
-}
-
-// Roulette over non-negative weights held one per lane (index = base + lane,
-// n indices in total, over JPL register chunks): pick = bounded(word, total),
-// result = the first index whose inclusive prefix exceeds pick; all-zero
-// weights fall back to a uniform index.
-template <int JPL>
-__device__ inline int roulette_chunks(const int64_t (&w)[JPL], int n, uint64_t word,
-                                      int64_t total) {
-    if (total == 0) return (int)bounded(word, (uint64_t)n);
-    const uint64_t pick = bounded(word, (uint64_t)total);
-    const int lane = lane_id();
-    int64_t carry = 0;
-#pragma unroll
-    for (int x = 0; x < JPL; ++x) {
-        if (x * kWave < n) {
-            const int h = x * kWave + lane;
-            const int64_t v = h < n ? w[x] : 0;
-            const int64_t incl = wave_incl_scan(v) + carry;
-            const uint64_t mask = __ballot(h < n && (uint64_t)incl > pick);
-            if (mask) return x * kWave + first_lane(mask);
-            carry = (int64_t)readlane64((uint64_t)incl, kWave - 1);
-        }
-    }
-    return n - 1;
-}
-
-__device__ inline int32_t clampi(int32_t v, int32_t lo, int32_t hi) {
-    return v < lo ? lo : (v > hi ? hi : v);
-}
-
-// #{x in pool[lo, hi) : x < v and x != skip}, uniform over the wave.
-__device__ inline int32_t seg_count_less(const int32_t *pool, int32_t lo, int32_t hi, int32_t v,
-                                         int32_t skip, int32_t limit) {
-    int32_t cnt = 0;
-    const int lane = lane_id();
-    lo = lo < 0 ? 0 : lo;
-    hi = hi > limit ? limit : hi;
-    for (int32_t b = lo; b < hi; b += kWave) {
-        const int32_t x = b + lane;
-        bool pred = false;
-        if (x < hi) {
-            const int32_t y = pool[x];
-            pred = (y < v) && (y != skip);
-        }
-        cnt += __popcll(__ballot(pred));
-    }
-    return cnt;
-}
-
-// Remove the element at `from`, insert v at `to`, shifting the elements in
-// between by one; every thread of the block takes part (uniform arguments).
-__device__ inline void pool_move(int32_t *pool, int32_t from, int32_t to, int32_t v) {
-    const int tid = threadIdx.x;
-    if (from < to) {
-        for (int32_t base = from; base < to; base += kThreads) {
-            const int32_t x = base + tid;
-            int32_t val = 0;
-            if (x < to) val = pool[x + 1];
-            __syncthreads();
-            if (x < to) pool[x] = val;
-            __syncthreads();
-        }
-    } else if (from > to) {
-        for (int32_t top = from; top > to; top -= kThreads) {
-            const int32_t x = top - tid;
-            int32_t val = 0;
-            if (x > to) val = pool[x - 1];
-            __syncthreads();
-            if (x > to) pool[x] = val;
-            __syncthreads();
-        }
-    }
-    if (tid == 0) pool[to] = v;
-    __syncthreads();
-}
-
-// Attention part A(r, g) = sum_s max_{x < count[g]} cost_s(cell x of the
-// row-shard), with up to two cells' statistics replaced.  Uniform over the
-// wave; requires count[g] <= 64.
-__device__ inline int64_t attention_rs(const AnnealArgs &a, const int64_t *T, const int64_t *Q,
-                                       int32_t r, int32_t g, int32_t c1, int64_t T1, int64_t Q1,
-                                       int32_t c2, int64_t T2, int64_t Q2) {
-    const int lane = lane_id();
-    const int32_t cnt = a.count[g];
-    const bool act = lane < cnt;
-    int64_t tv = 0, qv = 0;
-    if (act) {
-        const int32_t c = r * a.D + a.slots[g * a.D + lane];
-        if (c == c1) {
-            tv = T1;
-            qv = Q1;
-        } else if (c == c2) {
-            tv = T2;
-            qv = Q2;
-        } else {
-            tv = T[c];
-            qv = Q[c];
-        }
-    }
-    int64_t A = 0;
-    for (int s = 0; s < a.S; ++s) {
-        const int64_t cost = act ? a.alpha[s] * tv + a.beta[s] * qv : LLONG_MIN;
-        A += wave_max(cost);
-    }
-    return A;
-}
-
-__device__ inline int32_t seg_max32(int32_t v, int P) {
-    for (int d = 1; d < P; d <<= 1) {
-        const int32_t o = __shfl_xor(v, d, kWave);
-        v = o > v ? o : v;
-    }
-    return v;
-}
 
 template <bool WLDS>
 __global__ void __launch_bounds__(kThreads) k_anneal_level(AnnealArgs a) {
@@ -803,6 +651,11 @@ struct LevelEndArgs {
     uint64_t seed;
     int32_t level;
     int32_t init_mode;        // 1: x* := lowest-index argmin of results[.][0..2] (no comparison)
+    // in-place slabs: slab of each member now and after resampling, and the
+    // copies that give duplicated parents' extra children their state
+    const int32_t *slab_cur;  // [pop] or null (double-buffered slabs)
+    int32_t *slab_next;       // [pop]
+    int32_t *copy_src, *copy_dst, *n_copies;  // [pop], [pop], [1]
 };
 
 // After a level: the incumbent update (strict lexicographic improvement,
@@ -874,7 +727,9 @@ __global__ void __launch_bounds__(1024) k_level_end(LevelEndArgs a) {
         for (int j = tid; j < a.pop; j += blockDim.x) {
             if (a.parents_out) a.parents_out[j] = -1;
             a.next_parent[j] = j;
+            if (a.slab_cur) a.slab_next[j] = a.slab_cur[j];
         }
+        if (a.slab_cur && tid == 0) *a.n_copies = 0;
         return;
     }
     double emin = __builtin_inf();
@@ -949,6 +804,56 @@ __global__ void __launch_bounds__(1024) k_level_end(LevelEndArgs a) {
         a.next_parent[mm] = chosen;
         if (a.parents_out) a.parents_out[mm] = chosen;
     }
+    if (!a.slab_cur) return;
+    // Slab hand-over: parents are non-decreasing in m.  The first child of a
+    // parent takes over its slab; every further child takes the slab of a
+    // member without children (ascending order) after a copy.
+    __syncthreads();
+    const int32_t *par = a.next_parent;
+    int32_t n_dead = 0, n_dup = 0;
+    for (int j = lo; j < hi; ++j) {
+        int32_t l = 0, h = a.pop;  // lower bound of j in par
+        while (l < h) {
+            const int32_t md = (l + h) >> 1;
+            if (par[md] < j) l = md + 1;
+            else h = md;
+        }
+        n_dead += !(l < a.pop && par[l] == j);
+        n_dup += (j > 0 && par[j] == par[j - 1]);
+    }
+    __shared__ int32_t sdead[16], sdup[16];
+    const int32_t idead = (int32_t)wave_incl_scan(n_dead), idup = (int32_t)wave_incl_scan(n_dup);
+    if (lane == kWave - 1) {
+        sdead[wv] = idead;
+        sdup[wv] = idup;
+    }
+    __syncthreads();
+    int32_t rdead = idead - n_dead, rdup = idup - n_dup, tdup = 0;
+    for (int w = 0; w < wv; ++w) {
+        rdead += sdead[w];
+        rdup += sdup[w];
+    }
+    for (int w = 0; w < nw; ++w) tdup += sdup[w];
+    for (int j = lo; j < hi; ++j) {
+        int32_t l = 0, h = a.pop;
+        while (l < h) {
+            const int32_t md = (l + h) >> 1;
+            if (par[md] < j) l = md + 1;
+            else h = md;
+        }
+        if (!(l < a.pop && par[l] == j)) a.copy_dst[rdead++] = a.slab_cur[j];
+    }
+    __syncthreads();
+    for (int m2 = lo; m2 < hi; ++m2) {
+        if (m2 == 0 || par[m2] != par[m2 - 1]) {
+            a.slab_next[m2] = a.slab_cur[par[m2]];
+        } else {
+            a.slab_next[m2] = a.copy_dst[rdup];
+            a.copy_src[rdup] = a.slab_cur[par[m2]];
+            ++rdup;
+        }
+    }
+    if (tid == 0) *a.n_copies = tdup;
 }
 
 // population[m] = cell_of of slab parent[m] (or m).
@@ -1022,7 +927,6 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
     RP_TRY(upload_problem(prob, topo, scr, &dp, stream));
     const SlabOffsets off = slab_layout(N, B64, RG64, LP64);
     char *slabA = scr.get<char>((size_t)pop_size * off.bytes);
-    char *slabB = scr.get<char>((size_t)pop_size * off.bytes);
     int32_t *best = scr.get<int32_t>((size_t)pop_size * N);
     int64_t *results = scr.get<int64_t>((size_t)pop_size * kRes);
     int32_t *status = scr.get<int32_t>(pop_size + 1);
@@ -1119,14 +1023,44 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
     }
     (void)xscore_in;
 
+    // Kernel choice: one wave per member when its state fits LDS (members
+    // updated in place, slabs handed over at resampling), else one
+    // workgroup per member over double-buffered slabs.
+    int32_t mpw = 0;
+    bool tlds = false;
+    const char *force = getenv("ROUTEPACK_ANNEAL_KERNEL");
+    a.pop = pop_size;
+    const bool fast = !(force && strcmp(force, "workgroup") == 0) && wave_plan(a, &mpw, &tlds);
+    char *slabB = nullptr;
+    int32_t *slab_of[2] = {nullptr, nullptr};
+    int32_t *copy_src = nullptr, *copy_dst = nullptr, *n_copies = nullptr;
+    if (fast) {
+        slab_of[0] = scr.get<int32_t>(pop_size);
+        slab_of[1] = scr.get<int32_t>(pop_size);
+        copy_src = scr.get<int32_t>(pop_size);
+        copy_dst = scr.get<int32_t>(pop_size);
+        n_copies = scr.get<int32_t>(1);
+        if (scr.failed()) return ROUTEPACK_E_DEVICE;
+        std::vector<int32_t> iota(pop_size);
+        for (int j = 0; j < pop_size; ++j) iota[j] = j;
+        RP_HIP(hipMemcpyAsync(slab_of[0], iota.data(), sizeof(int32_t) * pop_size, hipMemcpyHostToDevice,
+                              stream));
+        RP_HIP(hipStreamSynchronize(stream));  // iota is a host temporary
+        a.slabs = slabA;
+        a.xscore = best_score;
+    } else {
+        slabB = scr.get<char>((size_t)pop_size * off.bytes);
+        if (scr.failed()) return ROUTEPACK_E_DEVICE;
+    }
     const size_t lds_w = (size_t)RG64 * LP64 * 4;
     const bool wlds = 128 + lds_w <= 160 * 1024;
     const size_t lds_level = 128 + (wlds ? lds_w : 0);
-    if (wlds)
+    if (!fast && wlds)
         RP_HIP(hipFuncSetAttribute((const void *)k_anneal_level<true>,
                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_level));
     char *src = slabA, *dst = slabB;
     const int32_t *cur_parent = nullptr;
+    int cur = 0;
     std::vector<hipEvent_t> ev;
     if (prm->level_kernel_ms) {
         ev.resize(2 * (size_t)prm->n_sweeps);
@@ -1137,17 +1071,22 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
         ~EventGuard() { for (auto e : v) (void)hipEventDestroy(e); }
     } ev_guard{ev};
     for (int n = 0; n < prm->n_sweeps; ++n) {
-        a.src = src;
-        a.dst = dst;
-        a.parent = cur_parent;
         a.level = prm->sweep_offset + n;
         a.temp = prm->temperatures[n];
         a.step_log = step_log ? step_log + (size_t)n * pop_size * a.K : nullptr;
         if (!ev.empty()) RP_HIP(hipEventRecord(ev[2 * n], stream));
-        if (wlds)
-            hipLaunchKernelGGL(k_anneal_level<true>, dim3(pop_size), dim3(kThreads), lds_level, stream, a);
-        else
-            hipLaunchKernelGGL(k_anneal_level<false>, dim3(pop_size), dim3(kThreads), lds_level, stream, a);
+        if (fast) {
+            a.slab_of = slab_of[cur];
+            RP_TRY(launch_anneal_wave(a, tlds, stream));
+        } else {
+            a.src = src;
+            a.dst = dst;
+            a.parent = cur_parent;
+            if (wlds)
+                hipLaunchKernelGGL(k_anneal_level<true>, dim3(pop_size), dim3(kThreads), lds_level, stream, a);
+            else
+                hipLaunchKernelGGL(k_anneal_level<false>, dim3(pop_size), dim3(kThreads), lds_level, stream, a);
+        }
         if (!ev.empty()) RP_HIP(hipEventRecord(ev[2 * n + 1], stream));
         const double t_after = (n + 1 < prm->n_sweeps) ? prm->temperatures[n + 1] : prm->t_next;
         le.src_slabs = src;
@@ -1157,15 +1096,32 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
         le.t_cur = prm->temperatures[n];
         le.t_next = t_after;
         le.level = a.level;
+        if (fast) {
+            le.slab_cur = slab_of[cur];
+            le.slab_next = slab_of[cur ^ 1];
+            le.copy_src = copy_src;
+            le.copy_dst = copy_dst;
+            le.n_copies = n_copies;
+        }
         hipLaunchKernelGGL(k_level_end, dim3(1), dim3(1024), 0, stream, le);
         RP_HIP(hipGetLastError());
-        cur_parent = parent;
-        std::swap(src, dst);
+        if (fast) {
+            RP_TRY(launch_copy_slabs(slabA, off.bytes, copy_src, copy_dst, n_copies, pop_size, stream));
+            cur ^= 1;
+        } else {
+            cur_parent = parent;
+            std::swap(src, dst);
+        }
     }
     // Output population: start states of the next level.
-    if (prm->n_sweeps > 0)
-        hipLaunchKernelGGL(k_gather_population, dim3(pop_size), dim3(256), 0, stream, src, off.bytes,
-                           off.cell, cur_parent, N, population);
+    if (prm->n_sweeps > 0) {
+        if (fast)
+            hipLaunchKernelGGL(k_gather_population, dim3(pop_size), dim3(256), 0, stream, slabA, off.bytes,
+                               off.cell, slab_of[cur], N, population);
+        else
+            hipLaunchKernelGGL(k_gather_population, dim3(pop_size), dim3(256), 0, stream, src, off.bytes,
+                               off.cell, cur_parent, N, population);
+    }
     RP_HIP(hipGetLastError());
     // Validate x* and the non-regression guarantee.
     RP_TRY(eval_layouts(prob, topo, dp, lengths, q, n_rows, 1, best_layout, chk_score, status,

@@ -108,58 +108,132 @@ __host__ __device__ inline bool lex_less(int64_t a0, int64_t a1, int64_t a2, int
 }
 
 // ---------------------------------------------------------------------------
-// wave64 collectives (every lane of the wave participates).
+// wave64 collectives (every lane of the wave participates).  Reductions and
+// scans use DPP row operations (16-lane rows) and combine the four rows with
+// readlane, so the full-wave results are uniform scalars; no LDS traffic.
 __device__ inline int lane_id() { return (int)(threadIdx.x & (kWave - 1)); }
 __device__ inline int wave_id() { return (int)(threadIdx.x / kWave); }
 
-__device__ inline int64_t wave_sum(int64_t v) {
-#pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, kWave);
+// DPP controls (GFX9 encoding).
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;  // reverse within 8 lanes
+constexpr int kDppMirror = 0x140;      // reverse within 16 lanes
+constexpr int kDppRowShr1 = 0x111;
+constexpr int kDppRowBcast15 = 0x142;
+constexpr int kDppRowBcast31 = 0x143;
+
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ inline int32_t dpp32(int32_t v, int32_t old) {
+    return __builtin_amdgcn_update_dpp(old, v, CTRL, ROW_MASK, 0xF, false);
+}
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ inline int64_t dpp64(int64_t v, int64_t old) {
+    const int32_t lo = dpp32<CTRL, ROW_MASK>((int32_t)(uint32_t)v, (int32_t)(uint32_t)old);
+    const int32_t hi = dpp32<CTRL, ROW_MASK>((int32_t)(uint32_t)((uint64_t)v >> 32),
+                                             (int32_t)(uint32_t)((uint64_t)old >> 32));
+    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+__device__ inline uint64_t readlane64(uint64_t v, int lane) {
+    const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+    const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), lane);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Row (16-lane) reductions: every lane ends with its row's result.
+__device__ inline int64_t row_max64(int64_t v) {
+    int64_t o;
+    o = dpp64<kDppXor1>(v, v); v = o > v ? o : v;
+    o = dpp64<kDppXor2>(v, v); v = o > v ? o : v;
+    o = dpp64<kDppHalfMirror>(v, v); v = o > v ? o : v;
+    o = dpp64<kDppMirror>(v, v); v = o > v ? o : v;
     return v;
+}
+__device__ inline int64_t row_min64(int64_t v) {
+    int64_t o;
+    o = dpp64<kDppXor1>(v, v); v = o < v ? o : v;
+    o = dpp64<kDppXor2>(v, v); v = o < v ? o : v;
+    o = dpp64<kDppHalfMirror>(v, v); v = o < v ? o : v;
+    o = dpp64<kDppMirror>(v, v); v = o < v ? o : v;
+    return v;
+}
+__device__ inline int64_t row_sum64(int64_t v) {
+    v += dpp64<kDppXor1>(v, 0);
+    v += dpp64<kDppXor2>(v, 0);
+    v += dpp64<kDppHalfMirror>(v, 0);
+    v += dpp64<kDppMirror>(v, 0);
+    return v;
+}
+
+__device__ inline int64_t wave_sum(int64_t v) {
+    v = row_sum64(v);
+    return (int64_t)(readlane64((uint64_t)v, 0) + readlane64((uint64_t)v, 16) +
+                     readlane64((uint64_t)v, 32) + readlane64((uint64_t)v, 48));
 }
 __device__ inline int64_t wave_max(int64_t v) {
-#pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) {
-        const int64_t o = __shfl_xor(v, d, kWave);
-        v = o > v ? o : v;
-    }
-    return v;
+    v = row_max64(v);
+    int64_t a = (int64_t)readlane64((uint64_t)v, 0), b = (int64_t)readlane64((uint64_t)v, 16);
+    int64_t c = (int64_t)readlane64((uint64_t)v, 32), d = (int64_t)readlane64((uint64_t)v, 48);
+    a = b > a ? b : a;
+    c = d > c ? d : c;
+    return c > a ? c : a;
 }
 __device__ inline int64_t wave_min(int64_t v) {
-#pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) {
-        const int64_t o = __shfl_xor(v, d, kWave);
-        v = o < v ? o : v;
-    }
-    return v;
+    v = row_min64(v);
+    int64_t a = (int64_t)readlane64((uint64_t)v, 0), b = (int64_t)readlane64((uint64_t)v, 16);
+    int64_t c = (int64_t)readlane64((uint64_t)v, 32), d = (int64_t)readlane64((uint64_t)v, 48);
+    a = b < a ? b : a;
+    c = d < c ? d : c;
+    return c < a ? c : a;
 }
 __device__ inline int32_t wave_max32(int32_t v) {
-#pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) {
-        const int32_t o = __shfl_xor(v, d, kWave);
-        v = o > v ? o : v;
-    }
-    return v;
+    int32_t o;
+    o = dpp32<kDppXor1>(v, v); v = o > v ? o : v;
+    o = dpp32<kDppXor2>(v, v); v = o > v ? o : v;
+    o = dpp32<kDppHalfMirror>(v, v); v = o > v ? o : v;
+    o = dpp32<kDppMirror>(v, v); v = o > v ? o : v;
+    int32_t a = __builtin_amdgcn_readlane(v, 0), b = __builtin_amdgcn_readlane(v, 16);
+    int32_t c = __builtin_amdgcn_readlane(v, 32), d = __builtin_amdgcn_readlane(v, 48);
+    a = b > a ? b : a;
+    c = d > c ? d : c;
+    return c > a ? c : a;
 }
-// inclusive prefix sum over lanes
+
+// Inclusive prefix sum over the 64 lanes: row scans by row_shr 1, 2, 4, 8,
+// then the row totals carried across rows by row_bcast15 and row_bcast31.
 __device__ inline int64_t wave_incl_scan(int64_t v) {
-    const int lane = lane_id();
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-        const int64_t o = __shfl_up(v, d, kWave);
-        if (lane >= d) v += o;
-    }
+    v += dpp64<kDppRowShr1>(v, 0);
+    v += dpp64<kDppRowShr1 + 1>(v, 0);
+    v += dpp64<kDppRowShr1 + 3>(v, 0);
+    v += dpp64<kDppRowShr1 + 7>(v, 0);
+    v += dpp64<kDppRowBcast15, 0xA>(v, 0);
+    v += dpp64<kDppRowBcast31, 0xC>(v, 0);
     return v;
 }
 __device__ inline uint64_t wave_incl_scan_u(uint64_t v) {
-    const int lane = lane_id();
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-        const uint64_t o = __shfl_up(v, d, kWave);
-        if (lane >= d) v += o;
+    return (uint64_t)wave_incl_scan((int64_t)v);
+}
+
+// Maximum over aligned groups of P adjacent lanes (P a power of two <= 64);
+// every lane of a group ends with the group's maximum.
+__device__ inline int32_t seg_max32(int32_t v, int P) {
+    int32_t o;
+    if (P >= 2) { o = dpp32<kDppXor1>(v, v); v = o > v ? o : v; }
+    if (P >= 4) { o = dpp32<kDppXor2>(v, v); v = o > v ? o : v; }
+    if (P >= 8) { o = dpp32<kDppHalfMirror>(v, v); v = o > v ? o : v; }
+    if (P >= 16) { o = dpp32<kDppMirror>(v, v); v = o > v ? o : v; }
+    if (P >= 32) {  // swap 16-lane halves of each 32-lane group
+        o = __builtin_amdgcn_ds_swizzle(v, 0x401F);
+        v = o > v ? o : v;
+    }
+    if (P >= 64) {
+        o = __shfl_xor(v, 32, kWave);
+        v = o > v ? o : v;
     }
     return v;
 }
+
 __device__ inline int first_lane(uint64_t mask) { return mask ? __ffsll((long long)mask) - 1 : -1; }
 
 }  // namespace rp

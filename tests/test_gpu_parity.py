@@ -112,12 +112,24 @@ def _compare_anneal(g, o, steps=False):
         assert np.array_equal(g["steps"].cpu().numpy(), o["steps"])
 
 
+KERNELS = ["wave", "workgroup"]
+
+
+def _use_kernel(monkeypatch, kernel):
+    if kernel == "workgroup":
+        monkeypatch.setenv("ROUTEPACK_ANNEAL_KERNEL", "workgroup")
+    else:
+        monkeypatch.delenv("ROUTEPACK_ANNEAL_KERNEL", raising=False)
+
+
 @gpu
+@pytest.mark.parametrize("kernel", KERNELS)
 @pytest.mark.parametrize("G", [1, 2])
-def test_anneal_full_trajectory_tiny(G):
+def test_anneal_full_trajectory_tiny(G, kernel, monkeypatch):
     import oracle as O
     rp = _rp()
-    _log(f"anneal tiny G={G} full schedule")
+    _use_kernel(monkeypatch, kernel)
+    _log(f"anneal tiny G={G} full schedule, {kernel} kernel")
     w, pd, pb, agg, slot, load, q = _window("tiny", G)
     pr = _packed("tiny", G)
     temps = synth.anneal_temperatures(w.levels)
@@ -131,15 +143,17 @@ def test_anneal_full_trajectory_tiny(G):
 
 
 @gpu
+@pytest.mark.parametrize("kernel", KERNELS)
 @pytest.mark.parametrize("G", [1, 4])
-def test_anneal_small_levels(G):
+def test_anneal_small_levels(G, kernel, monkeypatch):
     import oracle as O
     rp = _rp()
+    _use_kernel(monkeypatch, kernel)
     w, pd, pb, agg, slot, load, q = _window("small", G)
     pr = _packed("small", G)
     temps = synth.anneal_temperatures(w.levels)[:40]
     K = synth.windows.STEPS_PER_LEVEL
-    _log(f"anneal small G={G} 40 levels")
+    _log(f"anneal small G={G} 40 levels, {kernel} kernel")
     o = O.anneal(pb, w.lengths, q, pr["r_star"], pr["population"], temps, K, w.seed_anneal,
                  t_next=synth.anneal_temperatures(w.levels)[40])
     assert o["rc"] == 0
