@@ -32,9 +32,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-PMC_FILE = os.path.join(ROOT, "profiles", "anneal_level_mid_pmc.txt")
+PMC_FILE = os.path.join(ROOT, "profiles", "anneal_wave_mid_pmc.txt")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_12146_amd", "csrc", f)
-                  for f in ("rp_anneal.hip", "rp_device.h")]
+                  for f in ("rp_anneal_wave.hip", "rp_anneal.h", "rp_anneal.hip", "rp_device.h")]
 
 
 def kernel_source_hash() -> str:
@@ -210,7 +210,8 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": "k_anneal_wave", "avg_launch_ms": float(kms.mean()),
-                     "bytes_per_eval": bytes_per_eval},
+                     "bytes_per_eval": bytes_per_eval,
+                     "algorithmic_bytes_per_launch": evals * bytes_per_eval / len(kms)},
         "cpu_baseline": cpu,
         "attempted_per_s": attempted / dt,
         "evals_per_step": evals // args.steps,

@@ -50,7 +50,7 @@ struct AnnealArgs {
 };
 
 // Wave kernel plan and launchers (rp_anneal_wave.hip).
-bool wave_plan(AnnealArgs &a, int32_t *mpw_out, bool *tlds_out);
+bool wave_plan(AnnealArgs &a, int32_t n_cu, int32_t *mpw_out, bool *tlds_out);
 int launch_anneal_wave(const AnnealArgs &a, bool tlds, hipStream_t stream);
 int launch_copy_slabs(char *slabs, int64_t bytes, const int32_t *src, const int32_t *dst,
                       const int32_t *n_copies, int32_t pop, hipStream_t stream);

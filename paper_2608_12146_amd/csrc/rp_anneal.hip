@@ -1030,7 +1030,10 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
     bool tlds = false;
     const char *force = getenv("ROUTEPACK_ANNEAL_KERNEL");
     a.pop = pop_size;
-    const bool fast = !(force && strcmp(force, "workgroup") == 0) && wave_plan(a, &mpw, &tlds);
+    int dev = 0, n_cu = 256;
+    RP_HIP(hipGetDevice(&dev));
+    RP_HIP(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev));
+    const bool fast = !(force && strcmp(force, "workgroup") == 0) && wave_plan(a, n_cu, &mpw, &tlds);
     char *slabB = nullptr;
     int32_t *slab_of[2] = {nullptr, nullptr};
     int32_t *copy_src = nullptr, *copy_dst = nullptr, *n_copies = nullptr;

@@ -674,7 +674,7 @@ __global__ void __launch_bounds__(256) k_copy_slabs(char *slabs, int64_t bytes, 
 
 // Chooses the wave kernel's launch shape; returns false when a member's
 // state does not fit LDS (the caller then uses the workgroup kernel).
-bool wave_plan(AnnealArgs &a, int32_t *mpw_out, bool *tlds_out) {
+bool wave_plan(AnnealArgs &a, int32_t n_cu, int32_t *mpw_out, bool *tlds_out) {
     if (a.N > 65535 || a.B + 1 > 65535 || a.C > 2147483647LL || a.RG > kWave * 8) return false;
     auto up8 = [](int64_t x) { return (x + 7) & ~(int64_t)7; };
     int64_t o = 0;
@@ -689,12 +689,15 @@ bool wave_plan(AnnealArgs &a, int32_t *mpw_out, bool *tlds_out) {
     const int64_t lim = 160 * 1024;
     const int64_t base = up8(4 * ((int64_t)a.G * a.D + a.G + a.D));
     const int64_t with_t = up8(base + 4 * (int64_t)a.N);
-    int64_t mpw_t = (lim - with_t) / member, mpw_g = (lim - base) / member;
-    mpw_t = mpw_t > 8 ? 8 : mpw_t;
-    mpw_g = mpw_g > 8 ? 8 : mpw_g;
-    if (mpw_g < 1) return false;
-    const bool tlds = mpw_t >= mpw_g;
-    a.mpw = (int32_t)(tlds ? mpw_t : mpw_g);
+    const int64_t cap_g = (lim - base) / member, cap_t = (lim - with_t) / member;
+    if (cap_g < 1) return false;
+    // One member per wave, spread over every CU before any CU takes more:
+    // ceil(pop / CUs) members per workgroup, within LDS and 8 waves.
+    int64_t want = ((int64_t)a.pop + n_cu - 1) / n_cu;
+    want = want < 1 ? 1 : (want > 8 ? 8 : want);
+    bool tlds = cap_t >= want;
+    int64_t mpw = tlds ? want : (cap_g < want ? cap_g : want);
+    a.mpw = (int32_t)mpw;
     a.lds_shared = (int32_t)(tlds ? with_t : base);
     a.lds_member = (int32_t)member;
     *mpw_out = a.mpw;

@@ -55,6 +55,13 @@ __host__ __device__ inline U64x4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_
 // floor(w * m / 2^64): the multiply-shift bounded draw.
 __host__ __device__ inline uint64_t bounded(uint64_t w, uint64_t m) {
 #if defined(__HIP_DEVICE_COMPILE__)
+    if ((m >> 32) == 0) {
+        // m < 2^32: w m = hi(w) m 2^32 + lo(w) m, and adding
+        // floor(lo(w) m / 2^32) before the shift gives the same floor; both
+        // products are 32 x 32 -> 64 and the sum stays below 2^64.
+        const uint64_t a = (w >> 32) * m, b = (w & 0xFFFFFFFFull) * m;
+        return (a + (b >> 32)) >> 32;
+    }
     return __umul64hi(w, m);
 #else
     return (uint64_t)(((unsigned __int128)w * m) >> 64);
