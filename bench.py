@@ -14,7 +14,7 @@ experts, top-8 routing with a Zipf(1.2) profile drifting 10% per layer,
 
 Metric: annealing move-evals/s = evaluated (feasible) proposals of all
 levels and members, over the wall time of the steps.  The JSON line also
-carries the roofline of the dominant kernel (k_anneal_level) from HIP events
+carries the roofline of the dominant kernel (the annealing level kernel) from HIP events
 on the library's stream, and the CPU oracle timed on a bounded sample.
 """
 from __future__ import annotations
@@ -32,29 +32,42 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-PMC_FILE = os.path.join(ROOT, "profiles", "anneal_wave_mid_pmc.txt")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_12146_amd", "csrc", f)
-                  for f in ("rp_anneal_wave.hip", "rp_anneal.h", "rp_anneal.hip", "rp_device.h")]
+# Sources of each level kernel (its own file plus the shared annealing code).
+LEVEL_KERNEL_FILES = {
+    "chain": "rp_anneal_chain.hip",
+    "wave": "rp_anneal_wave.hip",
+    "workgroup": "rp_anneal.hip",
+}
 
 
-def kernel_source_hash() -> str:
+def kernel_sources(kernel):
+    files = sorted({LEVEL_KERNEL_FILES[kernel], "rp_anneal.h", "rp_anneal.hip", "rp_device.h"})
+    return [os.path.join(ROOT, "paper_2608_12146_amd", "csrc", f) for f in files]
+
+
+def pmc_file(kernel, window):
+    return os.path.join(ROOT, "profiles", f"anneal_{kernel}_{window}_pmc.txt")
+
+
+def kernel_source_hash(kernel) -> str:
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in kernel_sources(kernel):
         with open(f, "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def read_pmc():
-    """Counter-derived HBM traffic per dispatch, if taken on this kernel source."""
-    if not os.path.exists(PMC_FILE):
+def read_pmc(kernel, window):
+    """Counter-derived HBM traffic per dispatch, if taken on this kernel's sources."""
+    path = pmc_file(kernel, window)
+    if not os.path.exists(path):
         return None
     kv = {}
-    for line in open(PMC_FILE):
+    for line in open(path):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
-    if kv.get("kernel_source_sha256_16") != kernel_source_hash():
+    if kv.get("kernel_source_sha256_16") != kernel_source_hash(kernel):
         return None
     try:
         return float(kv["hbm_bytes_per_dispatch"])
@@ -137,6 +150,7 @@ def main():
         progress(f"warmup {k} {time.perf_counter() - t1:.2f} s")
     evals = acc = 0
     kernel_ms = []
+    level_kernel = None
     t0 = time.perf_counter()
     for _ in range(args.steps):
         q, load, pk, an = step()
@@ -144,12 +158,13 @@ def main():
         evals += int(tr[:, :, 7].sum().item())
         acc += int(tr[:, :, 6].sum().item())
         kernel_ms.append(an["level_kernel_ms"])
+        level_kernel = an["level_kernel"]
         progress(f"step done at {time.perf_counter() - t0:.2f} s")
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     attempted = args.steps * levels * w.pop * K
 
-    # Roofline of the level kernel (k_anneal_wave): algorithmic global bytes of an evaluated
+    # Roofline of the level kernel: algorithmic global bytes of an evaluated
     # move are the moved samples' q rows (2 L P int32 for a swap, L P for a
     # relocation), expected (2 - rho) L P 4 bytes at relocation rate rho.
     rho = W.RHO_U32 / 2.0**32
@@ -157,7 +172,7 @@ def main():
     kms = np.concatenate(kernel_ms)
     k_sec = float(kms.sum()) / 1e3
     achieved = evals * bytes_per_eval / k_sec / 1e9
-    traffic = read_pmc()
+    traffic = read_pmc(level_kernel, args.window)
 
     # Objective == oracle: the oracle rescoring of the GPU's x*, the oracle's
     # seed population, and one level of three members recomputed by the oracle.
@@ -209,7 +224,7 @@ def main():
         "config": {"workload": workload_text(w, args.edp), "levels": levels, "proposals_per_level": K},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "k_anneal_wave", "avg_launch_ms": float(kms.mean()),
+                     "kernel": "k_anneal_" + level_kernel, "avg_launch_ms": float(kms.mean()),
                      "bytes_per_eval": bytes_per_eval,
                      "algorithmic_bytes_per_launch": evals * bytes_per_eval / len(kms)},
         "cpu_baseline": cpu,

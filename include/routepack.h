@@ -138,7 +138,22 @@ typedef struct routepack_anneal_params {
     int32_t init_incumbent;      /* 1: x* := lowest-index argmin of the population */
     double *level_kernel_ms;     /* [host][n_sweeps] out or NULL: duration of each level's
                                     annealing kernel, from HIP events on `stream` */
+    int32_t *level_kernel;       /* [host] out or NULL: the level kernel that ran
+                                    (ROUTEPACK_KERNEL_*) */
 } routepack_anneal_params;
+
+/* Level kernels of routepack_anneal.  The library takes the first whose
+ * shape limits the problem meets; the environment variable
+ * ROUTEPACK_ANNEAL_KERNEL=chain|wave|workgroup requests one (a request the
+ * problem does not fit fails with ROUTEPACK_E_UNSUPPORTED).
+ *   CHAIN      one wave per member, lanes over (row-shard, layer) and cells:
+ *              P in {4, 8, 16}, L <= 32, R G <= 64, <= 16 slots per shard
+ *   WAVE       one wave per member, lanes over flat 64-entry strides:
+ *              R G <= 512, member state within LDS
+ *   WORKGROUP  one workgroup per member, state in HBM: every valid problem */
+#define ROUTEPACK_KERNEL_WORKGROUP 0
+#define ROUTEPACK_KERNEL_WAVE 1
+#define ROUTEPACK_KERNEL_CHAIN 2
 
 /* Fixed-row population annealing (Alg. 3) over n_sweeps levels.  Level n
  * (global index nn = sweep_offset + n) runs, for every member j independently,

@@ -20,6 +20,8 @@ ERRORS = {0: "ok", -1: "invalid argument", -2: "infeasible window", -3: "FixedRo
           -4: "infeasible layout", -5: "fixed-point overflow", -6: "HIP error",
           -7: "postcondition failed", -8: "unsupported size"}
 
+LEVEL_KERNELS = {0: "workgroup", 1: "wave", 2: "chain"}
+
 EXPORTS = ("routepack_aggregate_demand", "routepack_place_experts", "routepack_pack_rows",
            "routepack_anneal", "routepack_eval_objective", "routepack_strerror")
 
@@ -44,7 +46,7 @@ class _AnnealParams(C.Structure):
                 ("temperatures", C.POINTER(C.c_double)), ("t_next", C.c_double),
                 ("p_guide_u32", C.c_uint32), ("rho_u32", C.c_uint32), ("seed", C.c_uint64),
                 ("sweep_offset", C.c_int32), ("init_incumbent", C.c_int32),
-                ("level_kernel_ms", C.POINTER(C.c_double))]
+                ("level_kernel_ms", C.POINTER(C.c_double)), ("level_kernel", C.POINTER(C.c_int32))]
 
 
 _lib = None
@@ -195,14 +197,17 @@ def anneal(prob: Problem, lengths, q, n_rows, population, temperatures, steps_pe
     parents = torch.empty((ns, P), dtype=torch.int32, device="cuda") if want_parents else None
     steps = torch.empty((ns, P, steps_per_sweep), dtype=torch.uint8, device="cuda") if want_steps else None
     kms = np.zeros(max(ns, 1), dtype=np.float64) if kernel_times else None
+    used = C.c_int32(-1)
     ap = _AnnealParams(ns, steps_per_sweep, temps.ctypes.data_as(C.POINTER(C.c_double)), float(t_next),
                        p_guide_u32, rho_u32, seed, sweep_offset, 1 if init else 0,
-                       kms.ctypes.data_as(C.POINTER(C.c_double)) if kms is not None else None)
+                       kms.ctypes.data_as(C.POINTER(C.c_double)) if kms is not None else None,
+                       C.pointer(used))
     rc = lib.routepack_anneal(prob.ref, _ptr(t), _ptr(qq), n_rows, P, _ptr(popl), C.byref(ap), _ptr(bl),
                               _ptr(bs), _ptr(trace), _ptr(parents), _ptr(steps), _stream())
     _check("routepack_anneal", rc)
     return dict(population=popl, best_layout=bl, best_score=bs, trace=trace, parents=parents, steps=steps,
-                level_kernel_ms=None if kms is None else kms[:ns])
+                level_kernel_ms=None if kms is None else kms[:ns],
+                level_kernel=LEVEL_KERNELS.get(used.value))
 
 
 def eval_objective(prob: Problem, lengths, q, n_rows, layouts, rank_load=None, want_J=False,

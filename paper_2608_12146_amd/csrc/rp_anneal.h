@@ -46,12 +46,16 @@ struct AnnealArgs {
     int32_t pop, mpw;         // population, members per workgroup
     int32_t lds_shared, lds_member;
     int32_t o_cell, o_pool, o_start, o_T, o_Q, o_acost, o_Jpre;
+    int32_t o_Jpiv, o_tshared;  // chain kernel: J pivots (per member), lengths table (shared)
     unsigned long long *phase_cycles;  // [pop][8] with RP_PHASE_TIMERS builds, else unused
 };
 
 // Wave kernel plan and launchers (rp_anneal_wave.hip).
 bool wave_plan(AnnealArgs &a, int32_t n_cu, int32_t *mpw_out, bool *tlds_out);
 int launch_anneal_wave(const AnnealArgs &a, bool tlds, hipStream_t stream);
+// Chain kernel plan and launcher (rp_anneal_chain.hip).
+bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out, int32_t *dv_out);
+int launch_anneal_chain(const AnnealArgs &a, int32_t pv, int32_t dv, hipStream_t stream);
 int launch_copy_slabs(char *slabs, int64_t bytes, const int32_t *src, const int32_t *dst,
                       const int32_t *n_copies, int32_t pop, hipStream_t stream);
 

@@ -1024,16 +1024,27 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
     (void)xscore_in;
 
     // Kernel choice: one wave per member when its state fits LDS (members
-    // updated in place, slabs handed over at resampling), else one
-    // workgroup per member over double-buffered slabs.
-    int32_t mpw = 0;
+    // updated in place, slabs handed over at resampling) -- the chain kernel
+    // when the shape fits its lane layout, else the flat wave kernel --, else
+    // one workgroup per member over double-buffered slabs.
+    // ROUTEPACK_ANNEAL_KERNEL=chain|wave|workgroup requests one kernel; a
+    // request the problem does not fit fails with ROUTEPACK_E_UNSUPPORTED.
+    int32_t mpw = 0, chain_pv = 0, chain_dv = 0;
     bool tlds = false;
     const char *force = getenv("ROUTEPACK_ANNEAL_KERNEL");
+    const bool want_chain = !force || strcmp(force, "chain") == 0;
+    const bool want_wave = !force || strcmp(force, "wave") == 0;
+    const bool want_group = !force || strcmp(force, "workgroup") == 0;
+    if (!want_chain && !want_wave && !want_group) return ROUTEPACK_E_INVALID;
     a.pop = pop_size;
     int dev = 0, n_cu = 256;
     RP_HIP(hipGetDevice(&dev));
     RP_HIP(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev));
-    const bool fast = !(force && strcmp(force, "workgroup") == 0) && wave_plan(a, n_cu, &mpw, &tlds);
+    const bool chain = want_chain && chain_plan(a, n_cu, topo.max_count, &chain_pv, &chain_dv);
+    const bool fast = chain || (want_wave && wave_plan(a, n_cu, &mpw, &tlds));
+    if (!fast && !want_group) return ROUTEPACK_E_UNSUPPORTED;
+    if (prm->level_kernel)
+        *prm->level_kernel = chain ? ROUTEPACK_KERNEL_CHAIN : (fast ? ROUTEPACK_KERNEL_WAVE : ROUTEPACK_KERNEL_WORKGROUP);
     char *slabB = nullptr;
     int32_t *slab_of[2] = {nullptr, nullptr};
     int32_t *copy_src = nullptr, *copy_dst = nullptr, *n_copies = nullptr;
@@ -1080,7 +1091,8 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
         if (!ev.empty()) RP_HIP(hipEventRecord(ev[2 * n], stream));
         if (fast) {
             a.slab_of = slab_of[cur];
-            RP_TRY(launch_anneal_wave(a, tlds, stream));
+            if (chain) RP_TRY(launch_anneal_chain(a, chain_pv, chain_dv, stream));
+            else RP_TRY(launch_anneal_wave(a, tlds, stream));
         } else {
             a.src = src;
             a.dst = dst;

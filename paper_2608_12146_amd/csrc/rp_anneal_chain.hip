@@ -1,0 +1,728 @@
+// Fixed-row population annealing (Alg. 3), one wave per population member,
+// with the lanes laid out for the shape of one move rather than for a flat
+// 64-entry stride.
+//
+// Layout of a move's work over the 64 lanes:
+//  - W / q rows: lane (half, l) = (lane / 32, lane % 32) holds layer l of
+//    row-shard a (half 0) or b (half 1), all P ranks of that layer in
+//    registers, so the max over ranks is in-lane and only the sum over layers
+//    crosses lanes (one 16-lane DPP reduction per row-shard);
+//  - cells: lane (half, x) with x < 16 holds the x-th cell of the row-shard,
+//    so both attention maxima and both cell-cost prefixes come from one
+//    16-lane DPP pass.
+// Proposal screening is lane-parallel, as in the flat kernel, with a
+// search structure that needs a fixed, small number of dependent LDS reads:
+//  - the J roulette reads 8 pivots J_pre[8k+7] and then the 8 entries of one
+//    block (two reads instead of a six-step binary search);
+//  - the cell roulette reads the row-shard's cost prefix, stored
+//    contiguously per row-shard, in one vector of reads.
+// A relocation shifts the member pool through 32-bit words, four per lane
+// (one 16-byte LDS access), instead of one 16-bit element per lane.
+// The sequence of evaluated proposals, accept decisions and states is the
+// sequential one (a rejected proposal leaves every screen valid, an accepted
+// one triggers a re-screen of the rest of the batch).
+#include "rp_anneal.h"
+
+namespace rp {
+
+namespace {
+
+constexpr int64_t kInf = INT64_MAX;  // J prefix entries beyond the last row-shard
+
+__device__ inline void wsync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Inclusive prefix sum within each 16-lane row.
+__device__ inline int64_t row_incl_scan64(int64_t v) {
+    v += dpp64<kDppRowShr1>(v, 0);
+    v += dpp64<kDppRowShr1 + 1>(v, 0);
+    v += dpp64<kDppRowShr1 + 3>(v, 0);
+    v += dpp64<kDppRowShr1 + 7>(v, 0);
+    return v;
+}
+
+struct Lds {
+    uint16_t *cell, *pool, *start;
+    int32_t *T;
+    int64_t *Q, *Cp, *Jpre, *Jpiv;
+};
+
+struct Tables {
+    const int32_t *slots, *count, *shard, *soff, *t;
+};
+
+// Screen result of one proposal (per lane).
+struct Screen {
+    int32_t i, j, c1, c2, pos_i, pos_j, ti, tj;
+    bool feas;
+};
+
+__device__ inline int32_t clamp0(int32_t v, int32_t hi) { return v < 0 ? 0 : (v > hi ? hi : v); }
+
+// Resolves the proposal of this lane against the member's current state.
+template <int DV>
+__device__ inline Screen screen(const AnnealArgs &a, const Lds &M, const Tables &tb, uint64_t w0, uint64_t w1,
+                                uint64_t w2, uint64_t w3, uint64_t w4, uint64_t w5, uint64_t w6, int64_t s1,
+                                int64_t s2) {
+    Screen sc;
+    const int32_t N = a.N, B = a.B, RG = a.RG, D = a.D, G = a.G;
+    const bool guided = (uint32_t)w0 < a.p_guide;
+    const bool reloc = (uint32_t)(w0 >> 32) < a.rho;
+    // Uniform-mode indices (used by lanes whose proposal is not guided).
+    const int32_t ir = (int32_t)bounded(w1, (uint64_t)N);
+    const int32_t jr = (int32_t)bounded(w4, (uint64_t)N);
+    const int32_t cir = M.cell[ir], cjr = M.cell[jr];
+    const int32_t tir = tb.t[ir], tjr = tb.t[jr];
+    int32_t c1 = cir, c2 = reloc ? (int32_t)bounded(w4, (uint64_t)B) : cjr;
+    int32_t i = ir, j = reloc ? -1 : jr;
+    int32_t ti = tir, tj = reloc ? 0 : tjr;
+    sc.pos_i = -1;
+    sc.pos_j = -1;
+    if (__ballot(guided)) {
+        // Source row-shard: roulette over J; target: over s2 - J_h + 1.
+        const uint64_t pk1 = bounded(w1, (uint64_t)s1);
+        const int64_t sp1 = s2 + 1;
+        const uint64_t pk4 = bounded(w4, (uint64_t)((int64_t)RG * sp1 - s1));
+        int32_t k1 = 0, k4 = 0;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int64_t pv = M.Jpiv[k];
+            k1 += (uint64_t)pv <= pk1 ? 1 : 0;
+            k4 += (pv != kInf && (uint64_t)((int64_t)(8 * k + 8) * sp1 - pv) <= pk4) ? 1 : 0;
+        }
+        int32_t h1 = 8 * k1, h4 = 8 * k4;
+        const int64_t *f1 = M.Jpre + 8 * k1, *f4 = M.Jpre + 8 * k4;
+#pragma unroll
+        for (int x = 0; x < 8; ++x) {
+            const int64_t v1 = f1[x], v4 = f4[x];
+            h1 += (uint64_t)v1 <= pk1 ? 1 : 0;
+            h4 += (v4 != kInf && (uint64_t)((int64_t)(8 * k4 + x + 1) * sp1 - v4) <= pk4) ? 1 : 0;
+        }
+        if (s1 == 0) h1 = (int32_t)bounded(w1, (uint64_t)RG);
+        h1 = clamp0(h1, RG - 1);
+        h4 = clamp0(h4, RG - 1);
+        const int32_t r1 = h1 / G, g1 = h1 - r1 * G, r2 = h4 / G, g2 = h4 - r2 * G;
+        const int32_t cnt1 = tb.count[g1], cnt2 = tb.count[g2];
+        const int64_t *cp = M.Cp + r1 * D + tb.soff[g1];
+        int64_t cv[DV];
+#pragma unroll
+        for (int x = 0; x < DV; ++x) cv[x] = cp[x];
+        int64_t tot = 0;
+#pragma unroll
+        for (int x = 0; x < DV; ++x) tot = (x == cnt1 - 1) ? cv[x] : tot;
+        int32_t xi;
+        if (tot == 0) {
+            xi = (int32_t)bounded(w2, (uint64_t)cnt1);
+        } else {
+            const uint64_t pk2 = bounded(w2, (uint64_t)tot);
+            xi = 0;
+#pragma unroll
+            for (int x = 0; x < DV; ++x) xi += (x < cnt1 && (uint64_t)cv[x] <= pk2) ? 1 : 0;
+        }
+        xi = clamp0(xi, cnt1 - 1);
+        const int32_t x2 = (int32_t)bounded(w5, (uint64_t)cnt2);
+        const int32_t gc1 = clamp0(r1 * D + (G == 1 ? xi : tb.slots[g1 * D + xi]), B - 1);
+        const int32_t gc2 = clamp0(r2 * D + (G == 1 ? x2 : tb.slots[g2 * D + x2]), B - 1);
+        const int32_t st1 = M.start[gc1], en1 = M.start[gc1 + 1];
+        const int32_t st2 = M.start[gc2], en2 = M.start[gc2 + 1];
+        const int32_t pi = clamp0(st1 + (int32_t)bounded(w3, (uint64_t)(en1 - st1)), N - 1);
+        const int32_t pj = clamp0(st2 + (int32_t)bounded(w6, (uint64_t)(en2 - st2)), N - 1);
+        const int32_t gi = M.pool[pi], gj = M.pool[pj];
+        const int32_t gti = tb.t[gi], gtj = tb.t[gj];
+        if (guided) {
+            c1 = gc1;
+            c2 = gc2;
+            i = gi;
+            ti = gti;
+            sc.pos_i = pi;
+            if (!reloc) {
+                j = gj;
+                tj = gtj;
+                sc.pos_j = pj;
+            }
+        }
+    }
+    c1 = clamp0(c1, B - 1);
+    c2 = clamp0(c2, B - 1);
+    const int32_t T1 = M.T[c1], T2 = M.T[c2];
+    const int32_t sz1 = (int32_t)M.start[c1 + 1] - (int32_t)M.start[c1];
+    bool f = c1 != c2;
+    if (f) {
+        if (!reloc) f = ((int64_t)T1 - ti + tj <= a.C) && ((int64_t)T2 - tj + ti <= a.C);
+        else f = (sz1 >= 2) && ((int64_t)T2 + ti <= a.C);
+    }
+    sc.i = i;
+    sc.j = j;
+    sc.c1 = c1;
+    sc.c2 = c2;
+    sc.ti = ti;
+    sc.tj = tj;
+    sc.feas = f;
+    return sc;
+}
+
+// #{x in pool[lo, hi) : x < v and x != skip}, uniform over the wave.
+__device__ inline int32_t count_less(const uint16_t *pool, int32_t lo, int32_t hi, int32_t v, int32_t skip) {
+    int32_t cnt = 0;
+    const int lane = lane_id();
+    for (int32_t b = lo; b < hi; b += kWave) {
+        const int32_t x = b + lane;
+        bool pred = false;
+        if (x < hi) {
+            const int32_t y = pool[x];
+            pred = (y < v) && (y != skip);
+        }
+        cnt += __popcll(__ballot(pred));
+    }
+    return cnt;
+}
+
+// Removes the element at `from` and inserts v at `to`, shifting the elements
+// in between by one place, on 32-bit words, four per lane per step.  The
+// array is 16-byte aligned and padded by 16 bytes past its last word.
+__device__ inline void pool_move(uint16_t *pool16, int32_t from, int32_t to, uint32_t v) {
+    uint32_t *pw = reinterpret_cast<uint32_t *>(pool16);
+    const int lane = lane_id();
+    if (from < to) {
+        // new[x] = old[x + 1] for from <= x < to; new[to] = v
+        const int32_t wlast = to >> 1;
+        for (int32_t base = (from >> 1) & ~3; base <= wlast; base += 4 * kWave) {
+            const int32_t w = base + 4 * lane;
+            if (w <= wlast) {
+                const uint4 c = *reinterpret_cast<const uint4 *>(pw + w);
+                const uint32_t nx = pw[w + 4];
+                const uint32_t old[4] = {c.x, c.y, c.z, c.w};
+                const uint32_t nxt[4] = {c.y, c.z, c.w, nx};
+                uint32_t out[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int32_t e0 = 2 * (w + q), e1 = e0 + 1;
+                    const uint32_t sh = __builtin_amdgcn_alignbit(nxt[q], old[q], 16);
+                    const uint32_t lo = (e0 >= from && e0 < to) ? (sh & 0xFFFFu) : (e0 == to ? v : (old[q] & 0xFFFFu));
+                    const uint32_t hi = (e1 >= from && e1 < to) ? (sh >> 16) : (e1 == to ? v : (old[q] >> 16));
+                    out[q] = lo | (hi << 16);
+                }
+                *reinterpret_cast<uint4 *>(pw + w) = make_uint4(out[0], out[1], out[2], out[3]);
+            }
+            wsync();
+        }
+    } else if (from > to) {
+        // new[x] = old[x - 1] for to < x <= from; new[to] = v (high chunks first)
+        const int32_t wfirst = (to >> 1) & ~3;
+        for (int32_t top = (from >> 1) & ~3; top >= wfirst; top -= 4 * kWave) {
+            const int32_t w = top - 4 * lane;
+            if (w >= wfirst) {
+                const uint4 c = *reinterpret_cast<const uint4 *>(pw + w);
+                const uint32_t pv = w > 0 ? pw[w - 1] : 0u;
+                const uint32_t old[4] = {c.x, c.y, c.z, c.w};
+                const uint32_t prv[4] = {pv, c.x, c.y, c.z};
+                uint32_t out[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int32_t e0 = 2 * (w + q), e1 = e0 + 1;
+                    const uint32_t sh = __builtin_amdgcn_alignbit(old[q], prv[q], 16);
+                    const uint32_t lo = (e0 > to && e0 <= from) ? (sh & 0xFFFFu) : (e0 == to ? v : (old[q] & 0xFFFFu));
+                    const uint32_t hi = (e1 > to && e1 <= from) ? (sh >> 16) : (e1 == to ? v : (old[q] >> 16));
+                    out[q] = lo | (hi << 16);
+                }
+                *reinterpret_cast<uint4 *>(pw + w) = make_uint4(out[0], out[1], out[2], out[3]);
+            }
+            wsync();
+        }
+    } else {
+        if (lane == 0) pool16[to] = (uint16_t)v;
+        wsync();
+    }
+}
+
+// start[c] += d for lo < c <= hi (16-bit entries, 32-bit words four per lane).
+__device__ inline void start_add(uint16_t *start16, int32_t lo, int32_t hi, int32_t d) {
+    uint32_t *sw = reinterpret_cast<uint32_t *>(start16);
+    const int lane = lane_id();
+    const int32_t wlast = hi >> 1;
+    for (int32_t base = ((lo + 1) >> 1) & ~3; base <= wlast; base += 4 * kWave) {
+        const int32_t w = base + 4 * lane;
+        if (w <= wlast) {
+            const uint4 c = *reinterpret_cast<const uint4 *>(sw + w);
+            const uint32_t old[4] = {c.x, c.y, c.z, c.w};
+            uint32_t out[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int32_t e0 = 2 * (w + q), e1 = e0 + 1;
+                const uint32_t lo16 = (old[q] + ((e0 > lo && e0 <= hi) ? (uint32_t)d : 0u)) & 0xFFFFu;
+                const uint32_t hi16 = ((old[q] >> 16) + ((e1 > lo && e1 <= hi) ? (uint32_t)d : 0u)) & 0xFFFFu;
+                out[q] = lo16 | (hi16 << 16);
+            }
+            *reinterpret_cast<uint4 *>(sw + w) = make_uint4(out[0], out[1], out[2], out[3]);
+        }
+        wsync();
+    }
+}
+
+// J prefix over row-shards (lane h holds J_h) into LDS, with the pivot
+// entries J_pre[8k+7]; entries at h >= RG hold kInf.
+__device__ inline void write_jpre(const Lds &M, int64_t Jr, int32_t RG) {
+    const int lane = lane_id();
+    const int64_t incl = wave_incl_scan(lane < RG ? Jr : 0);
+    const int64_t v = lane < RG ? incl : kInf;
+    M.Jpre[lane] = v;
+    if ((lane & 7) == 7) M.Jpiv[lane >> 3] = v;
+}
+
+}  // namespace
+
+template <int PV, int DV>
+__global__ void __launch_bounds__(512) k_anneal_chain(AnnealArgs a) {
+    extern __shared__ __align__(16) char smem[];
+    const int lane = lane_id(), wv = wave_id();
+    const int32_t N = a.N, B = a.B, RG = a.RG, D = a.D, G = a.G, L = a.L;
+    int32_t *s_slots = reinterpret_cast<int32_t *>(smem);
+    int32_t *s_count = s_slots + G * D;
+    int32_t *s_shard = s_count + G;
+    int32_t *s_soff = s_shard + D;
+    int32_t *s_t = reinterpret_cast<int32_t *>(smem + a.o_tshared);
+    for (int32_t x = threadIdx.x; x < G * D; x += blockDim.x) s_slots[x] = a.slots[x];
+    for (int32_t x = threadIdx.x; x < G; x += blockDim.x) s_count[x] = a.count[x];
+    for (int32_t x = threadIdx.x; x < D; x += blockDim.x) s_shard[x] = a.slot_shard[x];
+    if (threadIdx.x == 0) {
+        int32_t acc = 0;
+        for (int32_t g = 0; g < G; ++g) {
+            s_soff[g] = acc;
+            acc += a.count[g];
+        }
+    }
+    {
+        const int32_t n4 = N >> 2;
+        const int4 *t4 = reinterpret_cast<const int4 *>(a.t);
+        for (int32_t x = threadIdx.x; x < n4; x += blockDim.x) reinterpret_cast<int4 *>(s_t)[x] = t4[x];
+        for (int32_t x = (n4 << 2) + threadIdx.x; x < N; x += blockDim.x) s_t[x] = a.t[x];
+    }
+    __syncthreads();
+    const int m = blockIdx.x * a.mpw + wv;
+    if (m >= a.pop) return;  // no block barrier follows
+    Tables tb{s_slots, s_count, s_shard, s_soff, s_t};
+    char *slab = a.slabs + (int64_t)a.slab_of[m] * a.off.bytes;
+    char *mine = smem + a.lds_shared + (int64_t)wv * a.lds_member;
+    Lds M;
+    M.cell = reinterpret_cast<uint16_t *>(mine + a.o_cell);
+    M.pool = reinterpret_cast<uint16_t *>(mine + a.o_pool);
+    M.start = reinterpret_cast<uint16_t *>(mine + a.o_start);
+    M.T = reinterpret_cast<int32_t *>(mine + a.o_T);
+    M.Q = reinterpret_cast<int64_t *>(mine + a.o_Q);
+    M.Cp = reinterpret_cast<int64_t *>(mine + a.o_acost);
+    M.Jpre = reinterpret_cast<int64_t *>(mine + a.o_Jpre);
+    M.Jpiv = reinterpret_cast<int64_t *>(mine + a.o_Jpiv);
+    int32_t *g_cell = at<int32_t>(slab, a.off.cell);
+    int32_t *g_pool = at<int32_t>(slab, a.off.pool);
+    int32_t *g_start = at<int32_t>(slab, a.off.start);
+    int64_t *g_T = at<int64_t>(slab, a.off.T);
+    int64_t *g_Q = at<int64_t>(slab, a.off.Q);
+    int32_t *W = at<int32_t>(slab, a.off.W);
+    int64_t *g_J = at<int64_t>(slab, a.off.J);
+    int64_t *g_A = at<int64_t>(slab, a.off.A);
+
+    // ---- prologue: member state into LDS and registers
+    {
+        const int32_t n4 = N >> 2;
+        const int4 *c4 = reinterpret_cast<const int4 *>(g_cell), *p4 = reinterpret_cast<const int4 *>(g_pool);
+        ushort4 *lc4 = reinterpret_cast<ushort4 *>(M.cell), *lp4 = reinterpret_cast<ushort4 *>(M.pool);
+#pragma unroll 4
+        for (int32_t x = lane; x < n4; x += kWave) {
+            const int4 u = c4[x], v = p4[x];
+            lc4[x] = make_ushort4((uint16_t)u.x, (uint16_t)u.y, (uint16_t)u.z, (uint16_t)u.w);
+            lp4[x] = make_ushort4((uint16_t)v.x, (uint16_t)v.y, (uint16_t)v.z, (uint16_t)v.w);
+        }
+        for (int32_t x = (n4 << 2) + lane; x < N; x += kWave) {
+            M.cell[x] = (uint16_t)g_cell[x];
+            M.pool[x] = (uint16_t)g_pool[x];
+        }
+    }
+#pragma unroll 4
+    for (int32_t x = lane; x <= B; x += kWave) M.start[x] = (uint16_t)g_start[x];
+#pragma unroll 4
+    for (int32_t x = lane; x < B; x += kWave) {
+        M.T[x] = (int32_t)g_T[x];
+        M.Q[x] = g_Q[x];
+    }
+    wsync();
+    // cost prefix of each row-shard's cells, in slot order (lanes over row-shards)
+    if (lane < RG) {
+        const int32_t r = lane / G, g = lane - (lane / G) * G;
+        int64_t acc = 0;
+        int64_t *cp = M.Cp + r * D + s_soff[g];
+        for (int32_t x = 0; x < s_count[g]; ++x) {
+            const int32_t c = r * D + s_slots[g * D + x];
+            const int64_t t = M.T[c], q = M.Q[c];
+            for (int s = 0; s < a.S; ++s) acc += a.alpha[s] * t + a.beta[s] * q;
+            cp[x] = acc;
+        }
+    }
+    int64_t Jr = lane < RG ? g_J[lane] : 0, Ar = lane < RG ? g_A[lane] : 0;
+    int64_t Ur = 0;
+    if (lane < G)
+        for (int r = 0; r < a.R; ++r) Ur += g_J[(int64_t)r * G + lane];
+    int64_t s0 = wave_max(lane < G ? Ur : LLONG_MIN);
+    int64_t s1 = wave_sum(lane < G ? Ur : 0);
+    int64_t s2 = wave_max(lane < RG ? Jr : LLONG_MIN);
+    write_jpre(M, Jr, RG);
+    wsync();
+    int64_t b0 = s0, b1 = s1, b2 = s2;
+    int32_t best_is_start = 1;
+    int32_t *bl = a.best + (int64_t)m * N;
+    const int64_t x0 = a.xscore[0], x1 = a.xscore[1], x2 = a.xscore[2];
+    if (lex_less(s0, s1, s2, x0, x1, x2)) {
+        for (int32_t x = lane; x < N; x += kWave) bl[x] = M.cell[x];
+        best_is_start = 0;
+    }
+    int64_t n_acc = 0, n_eval = 0;
+    double e_cur = energy(s0, s1, s2, a.scale);
+    uint8_t *log = a.step_log ? a.step_log + (int64_t)m * a.K : nullptr;
+    const int half = lane >> 5, hl = lane & 31, cx = lane & 15;
+    const bool lay_act = hl < L;  // lane holds layer hl of row-shard a / b
+    const bool cell_lane = (lane & 16) == 0;
+
+    for (int32_t k0 = 0; k0 < a.K; k0 += kWave) {
+        const int32_t k = k0 + lane;
+        const U64x4 b0w = philox4x64_10((uint64_t)k, (uint64_t)(uint32_t)a.level, (uint64_t)(uint32_t)m, 0,
+                                        a.seed, 0);
+        const U64x4 b1w = philox4x64_10((uint64_t)k, (uint64_t)(uint32_t)a.level, (uint64_t)(uint32_t)m, 1,
+                                        a.seed, 0);
+        const uint64_t w0 = b0w.v[0], w1 = b0w.v[1], w2 = b0w.v[2], w3 = b0w.v[3];
+        const uint64_t w4 = b1w.v[0], w5 = b1w.v[1], w6 = b1w.v[2], w7 = b1w.v[3];
+        uint64_t pending = __ballot(k < a.K);
+        Screen sc = screen<DV>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
+        uint64_t feas = __ballot(sc.feas && k < a.K);
+        while (pending) {
+            const uint64_t cand = pending & feas;
+            const uint64_t below = cand ? (cand & (~cand + 1)) - 1 : ~0ull;
+            if (log && ((pending & below) >> lane) & 1ull) log[k] = 0;
+            if (!cand) break;
+            const int f = first_lane(cand);
+            pending &= ~((cand & (~cand + 1)) | below);
+            // ---- evaluate proposal f (uniform)
+            const int32_t i = clamp0(__builtin_amdgcn_readlane(sc.i, f), N - 1);
+            const int32_t jf = __builtin_amdgcn_readlane(sc.j, f);
+            const int32_t j = jf < 0 ? -1 : clamp0(jf, N - 1);
+            const int32_t c1 = clamp0(__builtin_amdgcn_readlane(sc.c1, f), B - 1);
+            const int32_t c2 = clamp0(__builtin_amdgcn_readlane(sc.c2, f), B - 1);
+            int32_t pos_i = __builtin_amdgcn_readlane(sc.pos_i, f);
+            int32_t pos_j = __builtin_amdgcn_readlane(sc.pos_j, f);
+            const int64_t ti = __builtin_amdgcn_readlane(sc.ti, f);
+            const int64_t tj = __builtin_amdgcn_readlane(sc.tj, f);
+            const uint32_t fw0 = __builtin_amdgcn_readlane((int32_t)(uint32_t)(w0 >> 32), f);
+            const uint32_t fw7 = __builtin_amdgcn_readlane((int32_t)(uint32_t)(w7 >> 32), f);
+            const bool reloc = fw0 < a.rho;
+            n_eval += 1;
+            const int32_t ra = c1 / D, rb = c2 / D;
+            const int32_t ga = s_shard[c1 - ra * D], gb = s_shard[c2 - rb * D];
+            const int32_t ha = ra * G + ga, hb = rb * G + gb;
+            const bool two = ha != hb;
+            // W rows of a and b, q rows of i and j: issue the loads first.
+            int4 wr[PV / 4], qa[PV / 4], qb[PV / 4];
+            if (two) {
+                const int32_t row = half ? hb : ha, ll = lay_act ? hl : L - 1;
+                const int4 *wp = reinterpret_cast<const int4 *>(W + ((int64_t)row * L + ll) * PV);
+                const int4 *qip = reinterpret_cast<const int4 *>(a.q + ((int64_t)i * L + ll) * PV);
+                const int4 *qjp = reinterpret_cast<const int4 *>(a.q + ((int64_t)(j >= 0 ? j : i) * L + ll) * PV);
+#pragma unroll
+                for (int x = 0; x < PV / 4; ++x) {
+                    wr[x] = wp[x];
+                    qa[x] = qip[x];
+                    qb[x] = qjp[x];
+                }
+                if (j < 0) {
+#pragma unroll
+                    for (int x = 0; x < PV / 4; ++x) qb[x] = make_int4(0, 0, 0, 0);
+                }
+            }
+            // cell statistics of the two row-shards (lanes (half, cx))
+            const int32_t gsel = half ? gb : ga, rsel = half ? rb : ra;
+            const int32_t cnt = s_count[gsel];
+            const bool cact = cell_lane && cx < cnt && (half == 0 || two);
+            int64_t Tc = 0, Qc = 0;
+            int32_t cc = -1;
+            if (cact) {
+                cc = rsel * D + s_slots[gsel * D + cx];
+                Tc = M.T[cc];
+                Qc = M.Q[cc];
+                if (cc == c1) {
+                    Tc += tj - ti;
+                    Qc += tj * tj - ti * ti;
+                }
+                if (cc == c2) {  // (never the same cell as c1)
+                    Tc += ti - tj;
+                    Qc += ti * ti - tj * tj;
+                }
+            }
+            const int64_t T1 = M.T[c1], T2 = M.T[c2], Q1 = M.Q[c1], Q2v = M.Q[c2];
+            const int64_t nT1 = T1 - ti + tj, nT2 = T2 + ti - tj;
+            const int64_t nQ1 = Q1 - ti * ti + tj * tj, nQ2 = Q2v + ti * ti - tj * tj;
+            int64_t Arow = 0, cw = 0;
+            for (int s = 0; s < a.S; ++s) {
+                const int64_t cost = a.alpha[s] * Tc + a.beta[s] * Qc;
+                cw += cact ? cost : 0;
+                Arow = (int64_t)((uint64_t)Arow + (uint64_t)row_max64(cact ? cost : LLONG_MIN));
+            }
+            const int64_t Aa = (int64_t)readlane64((uint64_t)Arow, 0);
+            const int64_t Ab = two ? (int64_t)readlane64((uint64_t)Arow, 32) : Aa;
+            const int64_t Jha = (int64_t)readlane64((uint64_t)Jr, ha), Aha = (int64_t)readlane64((uint64_t)Ar, ha);
+            const int64_t Jhb = (int64_t)readlane64((uint64_t)Jr, hb);
+            int64_t Ja, Jb;
+            int32_t nw[PV];
+            if (two) {
+                int32_t mx = INT32_MIN;
+#pragma unroll
+                for (int x = 0; x < PV / 4; ++x) {
+                    const int32_t d0 = qa[x].x - qb[x].x, d1 = qa[x].y - qb[x].y;
+                    const int32_t d2 = qa[x].z - qb[x].z, d3 = qa[x].w - qb[x].w;
+                    nw[4 * x + 0] = half ? wr[x].x + d0 : wr[x].x - d0;
+                    nw[4 * x + 1] = half ? wr[x].y + d1 : wr[x].y - d1;
+                    nw[4 * x + 2] = half ? wr[x].z + d2 : wr[x].z - d2;
+                    nw[4 * x + 3] = half ? wr[x].w + d3 : wr[x].w - d3;
+                }
+#pragma unroll
+                for (int p = 0; p < PV; ++p) mx = nw[p] > mx ? nw[p] : mx;
+                const int64_t sm = row_sum64(lay_act ? (int64_t)mx : 0);
+                const int64_t suma = (int64_t)(readlane64((uint64_t)sm, 0) + readlane64((uint64_t)sm, 16));
+                const int64_t sumb = (int64_t)(readlane64((uint64_t)sm, 32) + readlane64((uint64_t)sm, 48));
+                Ja = Aa + (suma << a.F);
+                Jb = Ab + (sumb << a.F);
+            } else {
+                Ja = Aa + (Jha - Aha);
+                Jb = Ja;
+#pragma unroll
+                for (int p = 0; p < PV; ++p) nw[p] = 0;
+            }
+            const int64_t dJa = Ja - Jha, dJb = two ? Jb - Jhb : 0;
+            const int64_t n1 = s1 + dJa + dJb;
+            int64_t n0, Un = Ur;
+            if (G == 1) {
+                n0 = n1;
+                Un = n1;
+            } else {
+                if (lane == ga) Un += dJa;
+                if (lane == gb && two) Un += dJb;
+                n0 = wave_max(lane < G ? Un : LLONG_MIN);
+            }
+            const int64_t Jn = lane == ha ? Ja : (lane == hb ? Jb : Jr);
+            const int64_t n2 = wave_max(lane < RG ? Jn : LLONG_MIN);
+            const double e_new = energy(n0, n1, n2, a.scale);
+            bool accept = lex_less(n0, n1, n2, s0, s1, s2);
+            if (!accept) {
+                const double den = fabs(e_cur) > 1.0 ? fabs(e_cur) : 1.0;
+                const double delta = (e_new - e_cur) / den;
+                if (!(delta > 0.0)) {
+                    accept = true;  // z = 0 and exp(0) = 1 > u
+                } else {
+                    const double z = delta / a.temp;
+                    const double u = (double)fw7 * (1.0 / 4294967296.0);
+                    accept = u < exp_det(-z);
+                }
+            }
+            if (!accept) {
+                if (log && lane == f) log[k] = 1;
+                continue;  // the remaining screens stay valid
+            }
+            if (log && lane == f) log[k] = 2;
+            n_acc += 1;
+            // ---- commit
+            const int32_t st1 = M.start[c1], en1 = M.start[c1 + 1];
+            const int32_t st2 = M.start[c2], en2 = M.start[c2 + 1];
+            const int32_t sz1 = en1 - st1, sz2 = en2 - st2;
+            // members of both cells, half 0: c1, half 1: c2 (when both fit 32 lanes)
+            const bool small = sz1 <= 32 && sz2 <= 32;
+            int32_t y = -1;
+            bool yv = false;
+            if (small) {
+                const int32_t sz = half ? sz2 : sz1;
+                yv = hl < sz;
+                if (yv) y = M.pool[(half ? st2 : st1) + hl];
+            }
+            wsync();
+            if (two && lay_act) {
+                int4 *wp = reinterpret_cast<int4 *>(W + ((int64_t)(half ? hb : ha) * L + hl) * PV);
+#pragma unroll
+                for (int x = 0; x < PV / 4; ++x)
+                    wp[x] = make_int4(nw[4 * x], nw[4 * x + 1], nw[4 * x + 2], nw[4 * x + 3]);
+            }
+            if (!reloc) {
+                if (small) {
+                    // half 0: cell c1 drops i, takes j; half 1: cell c2 drops j, takes i
+                    const int32_t out = half ? j : i, in = half ? i : j;
+                    const uint64_t lt = __ballot(yv && y != out && y < in);
+                    const int32_t pin = __popcll(lt & (half ? 0xFFFFFFFF00000000ull : 0xFFFFFFFFull));
+                    const int32_t st = half ? st2 : st1;
+                    if (yv) {
+                        if (y == out) M.pool[st + pin] = (uint16_t)in;
+                        else M.pool[st + hl - (out < y ? 1 : 0) + (in < y ? 1 : 0)] = (uint16_t)y;
+                    }
+                    wsync();
+                } else {
+                    if (pos_i < 0) pos_i = st1 + count_less(M.pool, st1, en1, i, -1);
+                    if (pos_j < 0) pos_j = st2 + count_less(M.pool, st2, en2, j, -1);
+                    const int32_t to1 = st1 + count_less(M.pool, st1, en1, j, i);
+                    const int32_t to2 = st2 + count_less(M.pool, st2, en2, i, j);
+                    wsync();
+                    pool_move(M.pool, clamp0(pos_i, N - 1), clamp0(to1, N - 1), (uint32_t)j);
+                    pool_move(M.pool, clamp0(pos_j, N - 1), clamp0(to2, N - 1), (uint32_t)i);
+                }
+            } else {
+                int32_t rk;
+                if (small) {
+                    const uint64_t b1 = __ballot(yv && half == 0 && y < i);
+                    const uint64_t b2 = __ballot(yv && half == 1 && y < i);
+                    if (pos_i < 0) pos_i = st1 + __popcll(b1);
+                    rk = __popcll(b2);
+                } else {
+                    if (pos_i < 0) pos_i = st1 + count_less(M.pool, st1, en1, i, -1);
+                    rk = count_less(M.pool, st2, en2, i, -1);
+                }
+                const int32_t to = c1 < c2 ? st2 - 1 + rk : st2 + rk;
+                wsync();
+                pool_move(M.pool, clamp0(pos_i, N - 1), clamp0(to, N - 1), (uint32_t)i);
+                if (c1 < c2) start_add(M.start, c1, c2, -1);
+                else start_add(M.start, c2, c1, 1);
+            }
+            if (lane == 0) {
+                M.cell[i] = (uint16_t)c2;
+                if (j >= 0) M.cell[j] = (uint16_t)c1;
+                M.T[c1] = (int32_t)nT1;
+                M.Q[c1] = nQ1;
+                M.T[c2] = (int32_t)nT2;
+                M.Q[c2] = nQ2;
+            }
+            {
+                const int64_t incl = row_incl_scan64(cw);
+                if (cact) M.Cp[rsel * D + s_soff[gsel] + cx] = incl;
+            }
+            if (lane == ha) {
+                Jr = Ja;
+                Ar = Aa;
+            } else if (lane == hb) {
+                Jr = Jb;
+                Ar = Ab;
+            }
+            write_jpre(M, Jr, RG);
+            Ur = Un;
+            s0 = n0;
+            s1 = n1;
+            s2 = n2;
+            e_cur = e_new;
+            wsync();
+            if (lex_less(s0, s1, s2, b0, b1, b2)) {
+                b0 = s0;
+                b1 = s1;
+                b2 = s2;
+                best_is_start = 0;
+                if (lex_less(s0, s1, s2, x0, x1, x2))
+                    for (int32_t x = lane; x < N; x += kWave) bl[x] = M.cell[x];
+            }
+            if (pending) {
+                sc = screen<DV>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
+                feas = __ballot(sc.feas && k < a.K);
+            }
+        }
+    }
+    // ---- epilogue: the terminal state back to the slab
+    wsync();
+    {
+        const int32_t n4 = N >> 2;
+        int4 *c4 = reinterpret_cast<int4 *>(g_cell), *p4 = reinterpret_cast<int4 *>(g_pool);
+        const ushort4 *lc4 = reinterpret_cast<const ushort4 *>(M.cell), *lp4 = reinterpret_cast<const ushort4 *>(M.pool);
+        for (int32_t x = lane; x < n4; x += kWave) {
+            const ushort4 u = lc4[x], v = lp4[x];
+            c4[x] = make_int4(u.x, u.y, u.z, u.w);
+            p4[x] = make_int4(v.x, v.y, v.z, v.w);
+        }
+        for (int32_t x = (n4 << 2) + lane; x < N; x += kWave) {
+            g_cell[x] = M.cell[x];
+            g_pool[x] = M.pool[x];
+        }
+    }
+    for (int32_t x = lane; x <= B; x += kWave) g_start[x] = M.start[x];
+    for (int32_t x = lane; x < B; x += kWave) {
+        g_T[x] = M.T[x];
+        g_Q[x] = M.Q[x];
+    }
+    if (lane < RG) {
+        g_J[lane] = Jr;
+        g_A[lane] = Ar;
+    }
+    if (lane == 0) {
+        int64_t *res = a.results + (int64_t)m * kRes;
+        res[0] = s0; res[1] = s1; res[2] = s2;
+        res[3] = b0; res[4] = b1; res[5] = b2;
+        res[6] = n_acc; res[7] = n_eval;
+        res[8] = best_is_start;
+        res[9] = m;
+    }
+}
+
+// Launch shape of the chain kernel; false when the problem is outside its
+// shape (the caller then uses the flat wave kernel).
+bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out, int32_t *dv_out) {
+    const int32_t P = a.P;
+    if (!(P == 4 || P == 8 || P == 16)) return false;
+    if (a.L > 32 || a.RG > kWave || max_count > 16 || a.N > 65535 || a.B + 1 > 65535 || a.C > 2147483647LL)
+        return false;
+    const int32_t dv = max_count <= 8 ? 8 : 16;
+    auto up16 = [](int64_t x) { return (x + 15) & ~(int64_t)15; };
+    auto up8e = [](int64_t n) { return ((n + 7) & ~(int64_t)7) + 16; };  // elements, padded for 16-byte steps
+    int64_t o = 0;
+    a.o_cell = (int32_t)o; o = up16(o + 2 * (int64_t)a.N);
+    a.o_pool = (int32_t)o; o = up16(o + 2 * up8e(a.N));
+    a.o_start = (int32_t)o; o = up16(o + 2 * up8e((int64_t)a.B + 1));
+    a.o_T = (int32_t)o; o = up16(o + 4 * (int64_t)a.B);
+    a.o_Q = (int32_t)o; o = up16(o + 8 * (int64_t)a.B);
+    a.o_acost = (int32_t)o; o = up16(o + 8 * ((int64_t)a.B + dv));
+    a.o_Jpre = (int32_t)o; o = up16(o + 8 * 64);
+    a.o_Jpiv = (int32_t)o; o = up16(o + 8 * 8);
+    const int64_t member = o;
+    const int64_t tab = up16(4 * ((int64_t)a.G * a.D + 2 * a.G + a.D));
+    a.o_tshared = (int32_t)tab;
+    const int64_t shared = up16(tab + 4 * (int64_t)a.N);
+    const int64_t lim = 160 * 1024;
+    if (shared + member > lim) return false;
+    int64_t want = ((int64_t)a.pop + n_cu - 1) / n_cu;
+    want = want < 1 ? 1 : (want > 8 ? 8 : want);
+    const int64_t cap = (lim - shared) / member;
+    a.mpw = (int32_t)(want < cap ? want : cap);
+    a.lds_shared = (int32_t)shared;
+    a.lds_member = (int32_t)member;
+    *pv_out = P;
+    *dv_out = dv;
+    return true;
+}
+
+template <int PV, int DV>
+static int chain_launch_t(const AnnealArgs &a, hipStream_t stream) {
+    const size_t lds = (size_t)a.lds_shared + (size_t)a.mpw * a.lds_member;
+    if (hipFuncSetAttribute((const void *)k_anneal_chain<PV, DV>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)lds) != hipSuccess)
+        return ROUTEPACK_E_DEVICE;
+    const unsigned grid = (unsigned)((a.pop + a.mpw - 1) / a.mpw);
+    hipLaunchKernelGGL((k_anneal_chain<PV, DV>), dim3(grid), dim3(kWave * a.mpw), lds, stream, a);
+    return hipGetLastError() == hipSuccess ? ROUTEPACK_OK : ROUTEPACK_E_DEVICE;
+}
+
+int launch_anneal_chain(const AnnealArgs &a, int32_t pv, int32_t dv, hipStream_t stream) {
+    if (dv == 8) {
+        switch (pv) {
+            case 4: return chain_launch_t<4, 8>(a, stream);
+            case 8: return chain_launch_t<8, 8>(a, stream);
+            case 16: return chain_launch_t<16, 8>(a, stream);
+        }
+    } else {
+        switch (pv) {
+            case 4: return chain_launch_t<4, 16>(a, stream);
+            case 8: return chain_launch_t<8, 16>(a, stream);
+            case 16: return chain_launch_t<16, 16>(a, stream);
+        }
+    }
+    return ROUTEPACK_E_UNSUPPORTED;
+}
+
+}  // namespace rp

@@ -112,14 +112,12 @@ def _compare_anneal(g, o, steps=False):
         assert np.array_equal(g["steps"].cpu().numpy(), o["steps"])
 
 
-KERNELS = ["wave", "workgroup"]
+KERNELS = ["chain", "wave", "workgroup"]
 
 
 def _use_kernel(monkeypatch, kernel):
-    if kernel == "workgroup":
-        monkeypatch.setenv("ROUTEPACK_ANNEAL_KERNEL", "workgroup")
-    else:
-        monkeypatch.delenv("ROUTEPACK_ANNEAL_KERNEL", raising=False)
+    """Requests one annealing kernel; the library fails if the window does not fit it."""
+    monkeypatch.setenv("ROUTEPACK_ANNEAL_KERNEL", kernel)
 
 
 @gpu
@@ -139,12 +137,17 @@ def test_anneal_full_trajectory_tiny(G, kernel, monkeypatch):
     assert o["rc"] == 0
     g = rp.anneal(rp.Problem.from_dict(pd), w.lengths, q, pr["r_star"], pr["population"], temps, K,
                   w.seed_anneal, want_steps=True)
+    assert g["level_kernel"] == kernel
     _compare_anneal(g, o, steps=True)
+
+
+# The chain kernel holds one row-shard per lane (R* G <= 64 row-shards).
+CHAIN_MAX_ROW_SHARDS = 64
 
 
 @gpu
 @pytest.mark.parametrize("kernel", KERNELS)
-@pytest.mark.parametrize("G", [1, 4])
+@pytest.mark.parametrize("G", [1, 2, 4])
 def test_anneal_small_levels(G, kernel, monkeypatch):
     import oracle as O
     rp = _rp()
@@ -153,34 +156,56 @@ def test_anneal_small_levels(G, kernel, monkeypatch):
     pr = _packed("small", G)
     temps = synth.anneal_temperatures(w.levels)[:40]
     K = synth.windows.STEPS_PER_LEVEL
+    if kernel == "chain" and pr["r_star"] * G > CHAIN_MAX_ROW_SHARDS:
+        _log(f"anneal small G={G}: {pr['r_star'] * G} row-shards, chain kernel refuses")
+        with pytest.raises(rp.RoutepackError) as ei:
+            rp.anneal(rp.Problem.from_dict(pd), w.lengths, q, pr["r_star"], pr["population"], temps[:1], K,
+                      w.seed_anneal)
+        assert ei.value.code == -8
+        return
     _log(f"anneal small G={G} 40 levels, {kernel} kernel")
     o = O.anneal(pb, w.lengths, q, pr["r_star"], pr["population"], temps, K, w.seed_anneal,
                  t_next=synth.anneal_temperatures(w.levels)[40])
     assert o["rc"] == 0
     g = rp.anneal(rp.Problem.from_dict(pd), w.lengths, q, pr["r_star"], pr["population"], temps, K,
                   w.seed_anneal, t_next=synth.anneal_temperatures(w.levels)[40])
+    assert g["level_kernel"] == kernel
     _compare_anneal(g, o)
 
 
+@functools.lru_cache(maxsize=None)
+def _mid_oracle_levels():
+    """Oracle levels 0-1 of the mid window from the seed population."""
+    import oracle as O
+    w, pd, pb, agg, slot, load, q = _window("mid")
+    pr = _packed("mid")
+    temps = synth.anneal_temperatures(w.levels)
+    K = synth.windows.STEPS_PER_LEVEL
+    return O.anneal(pb, w.lengths, q, pr["r_star"], pr["population"], temps[:2], K, w.seed_anneal,
+                    t_next=temps[2])
+
+
 @gpu
-def test_anneal_mid_sampled_levels():
+@pytest.mark.parametrize("kernel", ["chain", "wave"])
+def test_anneal_mid_sampled_levels(kernel, monkeypatch):
     """Mid window at its full population: two levels from the seeds, then one
     late level resumed from the GPU's population, each checked against the
     oracle on the same start states."""
     import oracle as O
     rp = _rp()
+    _use_kernel(monkeypatch, kernel)
     w, pd, pb, agg, slot, load, q = _window("mid")
     pr = _packed("mid")
     temps = synth.anneal_temperatures(w.levels)
     K = synth.windows.STEPS_PER_LEVEL
     prob = rp.Problem.from_dict(pd)
-    _log("anneal mid levels 0-1")
-    o = O.anneal(pb, w.lengths, q, pr["r_star"], pr["population"], temps[:2], K, w.seed_anneal,
-                 t_next=temps[2])
+    _log(f"anneal mid levels 0-1, {kernel} kernel")
+    o = _mid_oracle_levels()
     g = rp.anneal(prob, w.lengths, q, pr["r_star"], pr["population"], temps[:2], K, w.seed_anneal,
                   t_next=temps[2])
+    assert g["level_kernel"] == kernel
     _compare_anneal(g, o)
-    _log("anneal mid level 1500 resumed")
+    _log(f"anneal mid level 1500 resumed, {kernel} kernel")
     start = g["population"].cpu().numpy()
     o2 = O.anneal(pb, w.lengths, q, pr["r_star"], start, temps[1500:1501], K, w.seed_anneal,
                   t_next=temps[1501], sweep_offset=1500, best_layout=o["best_layout"],
@@ -189,6 +214,38 @@ def test_anneal_mid_sampled_levels():
                    t_next=temps[1501], sweep_offset=1500, best_layout=g["best_layout"],
                    best_score=g["best_score"])
     _compare_anneal(g2, o2)
+
+
+@gpu
+@pytest.mark.parametrize("kernel", KERNELS)
+@pytest.mark.parametrize("G", [1, 2])
+def test_anneal_crowded_cells(G, kernel, monkeypatch):
+    """Hundreds of short samples per cell: member lists longer than a wave,
+    pool shifts that span several 512-entry steps, full trajectories with
+    step logs."""
+    import oracle as O
+    rp = _rp()
+    _use_kernel(monkeypatch, kernel)
+    w = synth.make_tiny_random(31 + G, n=2000, layers=4, experts=8, top_k=2, ranks=4, dp=2 * G,
+                               edp=G, cap=2048, tmin=1, tmax=10, pop=16, levels=12)
+    pd = synth.window_problem(w)
+    pb = O.Problem.from_dict(pd)
+    agg = O.aggregate(w.demand)
+    slot, load = O.place(agg, w.n_ranks)
+    q = O.project(w.demand, slot, w.n_ranks)
+    pr = O.pack_rows(pb, w.lengths, q, w.seed_pack, 8, 4, w.pop)
+    assert pr["rc"] == 0
+    sizes = np.bincount(pr["population"][0], minlength=pr["r_star"] * w.n_dp)
+    assert sizes.max() > 64
+    _log(f"anneal crowded G={G} (cells up to {sizes.max()} samples), {kernel} kernel")
+    temps = synth.anneal_temperatures(w.levels)
+    prob = rp.Problem.from_dict(pd)
+    o = O.anneal(pb, w.lengths, q, pr["r_star"], pr["population"], temps, 256, w.seed_anneal,
+                 want_steps=True)
+    g = rp.anneal(prob, w.lengths, q, pr["r_star"], pr["population"], temps, 256, w.seed_anneal,
+                  want_steps=True)
+    assert g["level_kernel"] == kernel
+    _compare_anneal(g, o, steps=True)
 
 
 @gpu
