@@ -137,15 +137,21 @@ typedef struct routepack_anneal_params {
     int32_t sweep_offset;        /* global index of this call's first level */
     int32_t init_incumbent;      /* 1: x* := lowest-index argmin of the population */
     double *level_kernel_ms;     /* [host][n_sweeps] out or NULL: duration of each level's
-                                    annealing kernel, from HIP events on `stream` */
+                                    annealing kernel, from HIP events on `stream`; with
+                                    ROUTEPACK_KERNEL_CHAIN_RUN (one kernel for all levels)
+                                    every entry is that kernel's duration / n_sweeps */
     int32_t *level_kernel;       /* [host] out or NULL: the level kernel that ran
                                     (ROUTEPACK_KERNEL_*) */
 } routepack_anneal_params;
 
 /* Level kernels of routepack_anneal.  The library takes the first whose
  * shape limits the problem meets; the environment variable
- * ROUTEPACK_ANNEAL_KERNEL=chain|wave|workgroup requests one (a request the
+ * ROUTEPACK_ANNEAL_KERNEL=chain_run|chain|wave|workgroup requests one (a request the
  * problem does not fit fails with ROUTEPACK_E_UNSUPPORTED).
+ *   CHAIN_RUN  the CHAIN kernel for every level in one cooperative launch
+ *              (member state stays on chip between levels; the level ends
+ *              run in the same kernel): CHAIN shapes whose workgroups can
+ *              all be resident at once
  *   CHAIN      one wave per member, lanes over (row-shard, layer) and cells:
  *              P in {4, 8, 16}, L <= 32, R G <= 64, <= 16 slots per shard
  *   WAVE       one wave per member, lanes over flat 64-entry strides:
@@ -154,6 +160,7 @@ typedef struct routepack_anneal_params {
 #define ROUTEPACK_KERNEL_WORKGROUP 0
 #define ROUTEPACK_KERNEL_WAVE 1
 #define ROUTEPACK_KERNEL_CHAIN 2
+#define ROUTEPACK_KERNEL_CHAIN_RUN 3
 
 /* Fixed-row population annealing (Alg. 3) over n_sweeps levels.  Level n
  * (global index nn = sweep_offset + n) runs, for every member j independently,

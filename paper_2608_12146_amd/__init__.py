@@ -20,7 +20,7 @@ ERRORS = {0: "ok", -1: "invalid argument", -2: "infeasible window", -3: "FixedRo
           -4: "infeasible layout", -5: "fixed-point overflow", -6: "HIP error",
           -7: "postcondition failed", -8: "unsupported size"}
 
-LEVEL_KERNELS = {0: "workgroup", 1: "wave", 2: "chain"}
+LEVEL_KERNELS = {0: "workgroup", 1: "wave", 2: "chain", 3: "chain_run"}
 
 EXPORTS = ("routepack_aggregate_demand", "routepack_place_experts", "routepack_pack_rows",
            "routepack_anneal", "routepack_eval_objective", "routepack_strerror")

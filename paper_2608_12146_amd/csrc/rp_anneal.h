@@ -53,9 +53,30 @@ struct AnnealArgs {
 // Wave kernel plan and launchers (rp_anneal_wave.hip).
 bool wave_plan(AnnealArgs &a, int32_t n_cu, int32_t *mpw_out, bool *tlds_out);
 int launch_anneal_wave(const AnnealArgs &a, bool tlds, hipStream_t stream);
-// Chain kernel plan and launcher (rp_anneal_chain.hip).
+// Arguments of the whole-schedule chain kernel (rp_anneal_chain.hip).
+struct RunArgs {
+    const double *temps;   // [n_sweeps] (device)
+    int32_t n_sweeps, offset;
+    double t_after;        // temperature after the last level; <= 0: no resampling after it
+    int64_t *trace;        // [n_sweeps][pop][8] or null
+    int32_t *parents_out;  // [n_sweeps][pop] or null
+    uint8_t *step_log;     // [n_sweeps][pop][K] or null
+    int32_t *xstar;        // [N]
+    int64_t *xscore;       // [3]
+    unsigned *bar;         // grid barrier arrivals (zero at launch)
+    int32_t *err;          // set when a grid barrier times out
+    int32_t *slab_of_out;  // [pop] slab of each member after the run
+    double *energy;        // [pop] terminal energy of each member (per level)
+    int64_t *wg_best;      // [workgroups][4] lexicographic-min trajectory best and its member
+    double *wg_emin;       // [workgroups] minimum terminal energy
+    int32_t o_lend;        // LDS offset of the level-end tables
+};
+
+// Chain kernel plan and launchers (rp_anneal_chain.hip).
 bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out, int32_t *dv_out);
 int launch_anneal_chain(const AnnealArgs &a, int32_t pv, int32_t dv, hipStream_t stream);
+int chain_run(const AnnealArgs &a, const RunArgs &r, int32_t pv, int32_t dv, int32_t n_cu, bool launch,
+              hipStream_t stream);
 int launch_copy_slabs(char *slabs, int64_t bytes, const int32_t *src, const int32_t *dst,
                       const int32_t *n_copies, int32_t pop, hipStream_t stream);
 

@@ -656,12 +656,14 @@ struct LevelEndArgs {
     const int32_t *slab_cur;  // [pop] or null (double-buffered slabs)
     int32_t *slab_next;       // [pop]
     int32_t *copy_src, *copy_dst, *n_copies;  // [pop], [pop], [1]
+    int32_t stage_lds;        // hand-over bookkeeping in dynamic LDS (3 pop int32)
 };
 
 // After a level: the incumbent update (strict lexicographic improvement,
 // ascending member order), the trace, and systematic resampling of the
 // terminal states with quantised Boltzmann weights.  One workgroup.
 __global__ void __launch_bounds__(1024) k_level_end(LevelEndArgs a) {
+    extern __shared__ int32_t lend_par[];  // [3 pop] when a.stage_lds: parents, flags, freed slabs
     __shared__ int64_t sk[16][4];
     __shared__ uint64_t su[16];
     __shared__ double sd[16];
@@ -803,12 +805,59 @@ __global__ void __launch_bounds__(1024) k_level_end(LevelEndArgs a) {
         }
         a.next_parent[mm] = chosen;
         if (a.parents_out) a.parents_out[mm] = chosen;
+        if (a.stage_lds) lend_par[mm] = chosen;
     }
     if (!a.slab_cur) return;
     // Slab hand-over: parents are non-decreasing in m.  The first child of a
     // parent takes over its slab; every further child takes the slab of a
     // member without children (ascending order) after a copy.
     __syncthreads();
+    if (a.stage_lds) {
+        // Parents, has-child flags and the freed slabs in LDS: every test is O(1).
+        int32_t *flag = lend_par + a.pop, *freed = flag + a.pop;
+        for (int j = tid; j < a.pop; j += blockDim.x) flag[j] = 0;
+        __syncthreads();
+        for (int mm = tid; mm < a.pop; mm += blockDim.x) flag[lend_par[mm]] = 1;
+        __syncthreads();
+        int32_t n_dead = 0, n_dup = 0;
+        for (int j = lo; j < hi; ++j) {
+            n_dead += flag[j] == 0;
+            n_dup += (j > 0 && lend_par[j] == lend_par[j - 1]);
+        }
+        __shared__ int32_t tdead[16], tdupw[16];
+        const int32_t idead = (int32_t)wave_incl_scan(n_dead), idup = (int32_t)wave_incl_scan(n_dup);
+        if (lane == kWave - 1) {
+            tdead[wv] = idead;
+            tdupw[wv] = idup;
+        }
+        __syncthreads();
+        int32_t rdead = idead - n_dead, rdup = idup - n_dup, tdup = 0;
+        for (int w = 0; w < wv; ++w) {
+            rdead += tdead[w];
+            rdup += tdupw[w];
+        }
+        for (int w = 0; w < nw; ++w) tdup += tdupw[w];
+        for (int j = lo; j < hi; ++j)
+            if (flag[j] == 0) {
+                const int32_t sl = a.slab_cur[j];
+                freed[rdead] = sl;
+                a.copy_dst[rdead] = sl;
+                ++rdead;
+            }
+        __syncthreads();
+        for (int m2 = lo; m2 < hi; ++m2) {
+            const int32_t p2 = lend_par[m2];
+            if (m2 == 0 || p2 != lend_par[m2 - 1]) {
+                a.slab_next[m2] = a.slab_cur[p2];
+            } else {
+                a.slab_next[m2] = freed[rdup];
+                a.copy_src[rdup] = a.slab_cur[p2];
+                ++rdup;
+            }
+        }
+        if (tid == 0) *a.n_copies = tdup;
+        return;
+    }
     const int32_t *par = a.next_parent;
     int32_t n_dead = 0, n_dup = 0;
     for (int j = lo; j < hi; ++j) {
@@ -996,6 +1045,12 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
     }
     LevelEndArgs le;
     memset(&le, 0, sizeof(le));
+    const size_t lend_lds = (size_t)12 * pop_size;
+    const bool lend_stage = lend_lds <= 112 * 1024;
+    if (lend_stage && lend_lds > 0)
+        RP_HIP(hipFuncSetAttribute((const void *)k_level_end, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                   (int)lend_lds));
+    const size_t lend_shm = lend_stage ? lend_lds : 0;
     le.pop = pop_size; le.N = N; le.results = results; le.best = best;
     le.slab_bytes = off.bytes; le.off_cell = off.cell;
     le.xstar = best_layout; le.xscore = best_score;
@@ -1003,7 +1058,7 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
     if (prm->init_incumbent) {
         le.init_mode = 1;
         le.start_layouts = population;
-        hipLaunchKernelGGL(k_level_end, dim3(1), dim3(1024), 0, stream, le);
+        hipLaunchKernelGGL(k_level_end, dim3(1), dim3(1024), lend_shm, stream, le);
         RP_HIP(hipGetLastError());
         le.init_mode = 0;
         le.start_layouts = nullptr;
@@ -1032,19 +1087,32 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
     int32_t mpw = 0, chain_pv = 0, chain_dv = 0;
     bool tlds = false;
     const char *force = getenv("ROUTEPACK_ANNEAL_KERNEL");
+    const bool want_run = !force || strcmp(force, "chain_run") == 0;
     const bool want_chain = !force || strcmp(force, "chain") == 0;
     const bool want_wave = !force || strcmp(force, "wave") == 0;
     const bool want_group = !force || strcmp(force, "workgroup") == 0;
-    if (!want_chain && !want_wave && !want_group) return ROUTEPACK_E_INVALID;
+    if (!want_run && !want_chain && !want_wave && !want_group) return ROUTEPACK_E_INVALID;
     a.pop = pop_size;
-    int dev = 0, n_cu = 256;
+    int dev = 0, n_cu = 256, coop = 0;
     RP_HIP(hipGetDevice(&dev));
     RP_HIP(hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev));
-    const bool chain = want_chain && chain_plan(a, n_cu, topo.max_count, &chain_pv, &chain_dv);
-    const bool fast = chain || (want_wave && wave_plan(a, n_cu, &mpw, &tlds));
+    RP_HIP(hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev));
+    const bool chain_fits = (want_run || want_chain) && chain_plan(a, n_cu, topo.max_count, &chain_pv, &chain_dv);
+    RunArgs run;
+    memset(&run, 0, sizeof(run));
+    bool whole = false;
+    if (chain_fits && want_run && coop && prm->n_sweeps > 0) {
+        const int rc = chain_run(a, run, chain_pv, chain_dv, n_cu, false, stream);
+        if (rc != ROUTEPACK_OK && rc != ROUTEPACK_E_UNSUPPORTED) return rc;
+        whole = rc == ROUTEPACK_OK;
+    }
+    const bool chain = chain_fits && !whole && want_chain;
+    const bool fast = whole || chain || (want_wave && wave_plan(a, n_cu, &mpw, &tlds));
     if (!fast && !want_group) return ROUTEPACK_E_UNSUPPORTED;
     if (prm->level_kernel)
-        *prm->level_kernel = chain ? ROUTEPACK_KERNEL_CHAIN : (fast ? ROUTEPACK_KERNEL_WAVE : ROUTEPACK_KERNEL_WORKGROUP);
+        *prm->level_kernel = whole ? ROUTEPACK_KERNEL_CHAIN_RUN
+                                   : (chain ? ROUTEPACK_KERNEL_CHAIN
+                                            : (fast ? ROUTEPACK_KERNEL_WAVE : ROUTEPACK_KERNEL_WORKGROUP));
     char *slabB = nullptr;
     int32_t *slab_of[2] = {nullptr, nullptr};
     int32_t *copy_src = nullptr, *copy_dst = nullptr, *n_copies = nullptr;
@@ -1084,6 +1152,73 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
         std::vector<hipEvent_t> &v;
         ~EventGuard() { for (auto e : v) (void)hipEventDestroy(e); }
     } ev_guard{ev};
+    if (whole) {
+        // The whole schedule in one cooperative launch.
+        double *temps_d = scr.get<double>(prm->n_sweeps);
+        unsigned *bar = scr.get<unsigned>(2);
+        int32_t *slab_final = scr.get<int32_t>(pop_size);
+        double *energy_d = scr.get<double>(pop_size);
+        int64_t *wg_best = scr.get<int64_t>((size_t)4 * pop_size);
+        double *wg_emin = scr.get<double>(pop_size);
+        if (scr.failed()) return ROUTEPACK_E_DEVICE;
+        RP_HIP(hipMemcpyAsync(temps_d, prm->temperatures, sizeof(double) * prm->n_sweeps, hipMemcpyHostToDevice,
+                              stream));
+        RP_HIP(hipMemsetAsync(bar, 0, 2 * sizeof(unsigned), stream));
+        a.slabs = slabA;
+        a.xscore = best_score;
+        run.temps = temps_d;
+        run.n_sweeps = prm->n_sweeps;
+        run.offset = prm->sweep_offset;
+        run.t_after = prm->t_next;
+        run.trace = trace;
+        run.parents_out = parents;
+        run.step_log = step_log;
+        run.xstar = best_layout;
+        run.xscore = best_score;
+        run.bar = bar;
+        run.err = reinterpret_cast<int32_t *>(bar + 1);
+        run.slab_of_out = slab_final;
+        run.energy = energy_d;
+        run.wg_best = wg_best;
+        run.wg_emin = wg_emin;
+        hipEvent_t e0 = nullptr, e1 = nullptr;
+        if (prm->level_kernel_ms) {
+            RP_HIP(hipEventCreate(&e0));
+            RP_HIP(hipEventCreate(&e1));
+            RP_HIP(hipEventRecord(e0, stream));
+        }
+        const int rc = chain_run(a, run, chain_pv, chain_dv, n_cu, true, stream);
+        if (rc != ROUTEPACK_OK) {
+            if (e0) (void)hipEventDestroy(e0);
+            if (e1) (void)hipEventDestroy(e1);
+            return rc;
+        }
+        if (e1) RP_HIP(hipEventRecord(e1, stream));
+        hipLaunchKernelGGL(k_gather_population, dim3(pop_size), dim3(256), 0, stream, slabA, off.bytes, off.cell,
+                           slab_final, N, population);
+        RP_HIP(hipGetLastError());
+        RP_TRY(eval_layouts(prob, topo, dp, lengths, q, n_rows, 1, best_layout, chk_score, status, nullptr,
+                            nullptr, nullptr, stream));
+        hipLaunchKernelGGL(k_compare_score, dim3(1), dim3(64), 0, stream, chk_score, best_score, status, chk);
+        int32_t ok = 0, err = 0;
+        RP_HIP(hipMemcpyAsync(&ok, chk, sizeof(ok), hipMemcpyDeviceToHost, stream));
+        RP_HIP(hipMemcpyAsync(&err, run.err, sizeof(err), hipMemcpyDeviceToHost, stream));
+        RP_HIP(hipMemcpyAsync(hx, best_score, sizeof(hx), hipMemcpyDeviceToHost, stream));
+        RP_HIP(hipStreamSynchronize(stream));
+        if (e0) {
+            float ms = 0.0f;
+            const hipError_t et = hipEventElapsedTime(&ms, e0, e1);
+            (void)hipEventDestroy(e0);
+            (void)hipEventDestroy(e1);
+            if (et != hipSuccess) return ROUTEPACK_E_DEVICE;
+            // one kernel for every level: each entry gets an equal share
+            for (int n = 0; n < prm->n_sweeps; ++n) prm->level_kernel_ms[n] = ms / prm->n_sweeps;
+        }
+        if (err) return ROUTEPACK_E_DEVICE;
+        if (!ok) return ROUTEPACK_E_INTERNAL;
+        if (lex_less(ref[0], ref[1], ref[2], hx[0], hx[1], hx[2])) return ROUTEPACK_E_INTERNAL;
+        return ROUTEPACK_OK;
+    }
     for (int n = 0; n < prm->n_sweeps; ++n) {
         a.level = prm->sweep_offset + n;
         a.temp = prm->temperatures[n];
@@ -1111,6 +1246,7 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
         le.t_cur = prm->temperatures[n];
         le.t_next = t_after;
         le.level = a.level;
+        le.stage_lds = lend_stage ? 1 : 0;
         if (fast) {
             le.slab_cur = slab_of[cur];
             le.slab_next = slab_of[cur ^ 1];
@@ -1118,7 +1254,7 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
             le.copy_dst = copy_dst;
             le.n_copies = n_copies;
         }
-        hipLaunchKernelGGL(k_level_end, dim3(1), dim3(1024), 0, stream, le);
+        hipLaunchKernelGGL(k_level_end, dim3(1), dim3(1024), lend_shm, stream, le);
         RP_HIP(hipGetLastError());
         if (fast) {
             RP_TRY(launch_copy_slabs(slabA, off.bytes, copy_src, copy_dst, n_copies, pop_size, stream));

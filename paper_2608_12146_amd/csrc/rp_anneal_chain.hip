@@ -272,13 +272,37 @@ __device__ inline void write_jpre(const Lds &M, int64_t Jr, int32_t RG) {
     if ((lane & 7) == 7) M.Jpiv[lane >> 3] = v;
 }
 
-}  // namespace
+// Member state kept in registers between proposals: J and A of the
+// row-shard held by each lane, U of the EDP shard held by each lane, and the
+// current score.
+struct Regs {
+    int64_t Jr, Ar, Ur, s0, s1, s2;
+};
 
-template <int PV, int DV>
-__global__ void __launch_bounds__(512) k_anneal_chain(AnnealArgs a) {
-    extern __shared__ __align__(16) char smem[];
-    const int lane = lane_id(), wv = wave_id();
-    const int32_t N = a.N, B = a.B, RG = a.RG, D = a.D, G = a.G, L = a.L;
+// Member slab sections in HBM.
+struct SlabPtrs {
+    int32_t *cell, *pool, *start, *W;
+    int64_t *T, *Q, *J, *A;
+};
+
+__device__ inline SlabPtrs slab_ptrs(const AnnealArgs &a, char *slab) {
+    SlabPtrs g;
+    g.cell = at<int32_t>(slab, a.off.cell);
+    g.pool = at<int32_t>(slab, a.off.pool);
+    g.start = at<int32_t>(slab, a.off.start);
+    g.T = at<int64_t>(slab, a.off.T);
+    g.Q = at<int64_t>(slab, a.off.Q);
+    g.W = at<int32_t>(slab, a.off.W);
+    g.J = at<int64_t>(slab, a.off.J);
+    g.A = at<int64_t>(slab, a.off.A);
+    return g;
+}
+
+// Workgroup tables in LDS: the slot list, slot count and first cost-prefix
+// index of every EDP shard, the shard of every slot, and the lengths.
+// Every thread of the workgroup takes part (ends with a block barrier).
+__device__ inline Tables load_tables(const AnnealArgs &a, char *smem) {
+    const int32_t N = a.N, D = a.D, G = a.G;
     int32_t *s_slots = reinterpret_cast<int32_t *>(smem);
     int32_t *s_count = s_slots + G * D;
     int32_t *s_shard = s_count + G;
@@ -294,17 +318,15 @@ __global__ void __launch_bounds__(512) k_anneal_chain(AnnealArgs a) {
             acc += a.count[g];
         }
     }
-    {
-        const int32_t n4 = N >> 2;
-        const int4 *t4 = reinterpret_cast<const int4 *>(a.t);
-        for (int32_t x = threadIdx.x; x < n4; x += blockDim.x) reinterpret_cast<int4 *>(s_t)[x] = t4[x];
-        for (int32_t x = (n4 << 2) + threadIdx.x; x < N; x += blockDim.x) s_t[x] = a.t[x];
-    }
+    const int32_t n4 = N >> 2;
+    const int4 *t4 = reinterpret_cast<const int4 *>(a.t);
+    for (int32_t x = threadIdx.x; x < n4; x += blockDim.x) reinterpret_cast<int4 *>(s_t)[x] = t4[x];
+    for (int32_t x = (n4 << 2) + threadIdx.x; x < N; x += blockDim.x) s_t[x] = a.t[x];
     __syncthreads();
-    const int m = blockIdx.x * a.mpw + wv;
-    if (m >= a.pop) return;  // no block barrier follows
-    Tables tb{s_slots, s_count, s_shard, s_soff, s_t};
-    char *slab = a.slabs + (int64_t)a.slab_of[m] * a.off.bytes;
+    return Tables{s_slots, s_count, s_shard, s_soff, s_t};
+}
+
+__device__ inline Lds member_lds(const AnnealArgs &a, char *smem, int wv) {
     char *mine = smem + a.lds_shared + (int64_t)wv * a.lds_member;
     Lds M;
     M.cell = reinterpret_cast<uint16_t *>(mine + a.o_cell);
@@ -315,80 +337,161 @@ __global__ void __launch_bounds__(512) k_anneal_chain(AnnealArgs a) {
     M.Cp = reinterpret_cast<int64_t *>(mine + a.o_acost);
     M.Jpre = reinterpret_cast<int64_t *>(mine + a.o_Jpre);
     M.Jpiv = reinterpret_cast<int64_t *>(mine + a.o_Jpiv);
-    int32_t *g_cell = at<int32_t>(slab, a.off.cell);
-    int32_t *g_pool = at<int32_t>(slab, a.off.pool);
-    int32_t *g_start = at<int32_t>(slab, a.off.start);
-    int64_t *g_T = at<int64_t>(slab, a.off.T);
-    int64_t *g_Q = at<int64_t>(slab, a.off.Q);
-    int32_t *W = at<int32_t>(slab, a.off.W);
-    int64_t *g_J = at<int64_t>(slab, a.off.J);
-    int64_t *g_A = at<int64_t>(slab, a.off.A);
+    return M;
+}
 
-    // ---- prologue: member state into LDS and registers
+// A member's state from a slab into LDS and registers (one wave).  The
+// global loads go out in batches of 16 per lane per array before any LDS
+// store, so a reload costs few memory round trips.
+__device__ inline void member_load(const AnnealArgs &a, const Lds &M, const Tables &tb, const SlabPtrs &g,
+                                   Regs &R) {
+    const int lane = lane_id();
+    const int32_t N = a.N, B = a.B, RG = a.RG, D = a.D, G = a.G;
+    constexpr int U = 16;
     {
         const int32_t n4 = N >> 2;
-        const int4 *c4 = reinterpret_cast<const int4 *>(g_cell), *p4 = reinterpret_cast<const int4 *>(g_pool);
+        const int4 *c4 = reinterpret_cast<const int4 *>(g.cell), *p4 = reinterpret_cast<const int4 *>(g.pool);
         ushort4 *lc4 = reinterpret_cast<ushort4 *>(M.cell), *lp4 = reinterpret_cast<ushort4 *>(M.pool);
-#pragma unroll 4
-        for (int32_t x = lane; x < n4; x += kWave) {
-            const int4 u = c4[x], v = p4[x];
-            lc4[x] = make_ushort4((uint16_t)u.x, (uint16_t)u.y, (uint16_t)u.z, (uint16_t)u.w);
-            lp4[x] = make_ushort4((uint16_t)v.x, (uint16_t)v.y, (uint16_t)v.z, (uint16_t)v.w);
+        for (int32_t base = 0; base < n4; base += U * kWave) {
+            int4 cu[U], pu[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int32_t x = base + u * kWave + lane;
+                if (x < n4) {
+                    cu[u] = c4[x];
+                    pu[u] = p4[x];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int32_t x = base + u * kWave + lane;
+                if (x < n4) {
+                    lc4[x] = make_ushort4((uint16_t)cu[u].x, (uint16_t)cu[u].y, (uint16_t)cu[u].z, (uint16_t)cu[u].w);
+                    lp4[x] = make_ushort4((uint16_t)pu[u].x, (uint16_t)pu[u].y, (uint16_t)pu[u].z, (uint16_t)pu[u].w);
+                }
+            }
         }
         for (int32_t x = (n4 << 2) + lane; x < N; x += kWave) {
-            M.cell[x] = (uint16_t)g_cell[x];
-            M.pool[x] = (uint16_t)g_pool[x];
+            M.cell[x] = (uint16_t)g.cell[x];
+            M.pool[x] = (uint16_t)g.pool[x];
         }
     }
-#pragma unroll 4
-    for (int32_t x = lane; x <= B; x += kWave) M.start[x] = (uint16_t)g_start[x];
-#pragma unroll 4
-    for (int32_t x = lane; x < B; x += kWave) {
-        M.T[x] = (int32_t)g_T[x];
-        M.Q[x] = g_Q[x];
+    for (int32_t base = 0; base <= B; base += U * kWave) {
+        int32_t sv[U];
+        int64_t tv[U], qv[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int32_t x = base + u * kWave + lane;
+            if (x <= B) sv[u] = g.start[x];
+            if (x < B) {
+                tv[u] = g.T[x];
+                qv[u] = g.Q[x];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int32_t x = base + u * kWave + lane;
+            if (x <= B) M.start[x] = (uint16_t)sv[u];
+            if (x < B) {
+                M.T[x] = (int32_t)tv[u];
+                M.Q[x] = qv[u];
+            }
+        }
     }
+    R.Jr = lane < RG ? g.J[lane] : 0;
+    R.Ar = lane < RG ? g.A[lane] : 0;
     wsync();
     // cost prefix of each row-shard's cells, in slot order (lanes over row-shards)
     if (lane < RG) {
-        const int32_t r = lane / G, g = lane - (lane / G) * G;
+        const int32_t r = lane / G, gg = lane - (lane / G) * G;
         int64_t acc = 0;
-        int64_t *cp = M.Cp + r * D + s_soff[g];
-        for (int32_t x = 0; x < s_count[g]; ++x) {
-            const int32_t c = r * D + s_slots[g * D + x];
+        int64_t *cp = M.Cp + r * D + tb.soff[gg];
+        for (int32_t x = 0; x < tb.count[gg]; ++x) {
+            const int32_t c = r * D + tb.slots[gg * D + x];
             const int64_t t = M.T[c], q = M.Q[c];
             for (int s = 0; s < a.S; ++s) acc += a.alpha[s] * t + a.beta[s] * q;
             cp[x] = acc;
         }
     }
-    int64_t Jr = lane < RG ? g_J[lane] : 0, Ar = lane < RG ? g_A[lane] : 0;
+    // U_g = sum over rows of J(r, g); lane g holds it
     int64_t Ur = 0;
-    if (lane < G)
-        for (int r = 0; r < a.R; ++r) Ur += g_J[(int64_t)r * G + lane];
-    int64_t s0 = wave_max(lane < G ? Ur : LLONG_MIN);
-    int64_t s1 = wave_sum(lane < G ? Ur : 0);
-    int64_t s2 = wave_max(lane < RG ? Jr : LLONG_MIN);
-    write_jpre(M, Jr, RG);
+    const int32_t gl = lane - (lane / G) * G;
+    for (int32_t gg = 0; gg < G; ++gg) {
+        const int64_t u = wave_sum(lane < RG && gl == gg ? R.Jr : 0);
+        if (lane == gg) Ur = u;
+    }
+    R.Ur = Ur;
+    R.s0 = wave_max(lane < G ? Ur : LLONG_MIN);
+    R.s1 = wave_sum(lane < G ? Ur : 0);
+    R.s2 = wave_max(lane < RG ? R.Jr : LLONG_MIN);
+    write_jpre(M, R.Jr, RG);
     wsync();
+}
+
+// A member's state back to a slab (W is kept up to date in the slab).
+__device__ inline void member_store(const AnnealArgs &a, const Lds &M, const SlabPtrs &g, const Regs &R) {
+    const int lane = lane_id();
+    const int32_t N = a.N, B = a.B, RG = a.RG;
+    wsync();
+    const int32_t n4 = N >> 2;
+    int4 *c4 = reinterpret_cast<int4 *>(g.cell), *p4 = reinterpret_cast<int4 *>(g.pool);
+    const ushort4 *lc4 = reinterpret_cast<const ushort4 *>(M.cell), *lp4 = reinterpret_cast<const ushort4 *>(M.pool);
+    for (int32_t x = lane; x < n4; x += kWave) {
+        const ushort4 u = lc4[x], v = lp4[x];
+        c4[x] = make_int4(u.x, u.y, u.z, u.w);
+        p4[x] = make_int4(v.x, v.y, v.z, v.w);
+    }
+    for (int32_t x = (n4 << 2) + lane; x < N; x += kWave) {
+        g.cell[x] = M.cell[x];
+        g.pool[x] = M.pool[x];
+    }
+    for (int32_t x = lane; x <= B; x += kWave) g.start[x] = M.start[x];
+    for (int32_t x = lane; x < B; x += kWave) {
+        g.T[x] = M.T[x];
+        g.Q[x] = M.Q[x];
+    }
+    if (lane < RG) {
+        g.J[lane] = R.Jr;
+        g.A[lane] = R.Ar;
+    }
+}
+
+// One level (K proposals) of member m from its current state, at the given
+// level index and temperature; x0..x2 is the incumbent score at the level
+// start.  Writes the member's result row.
+// Summary of a member's level for the level end.
+struct LevelOut {
+    int64_t b0, b1, b2;  // trajectory best
+    double e;            // terminal energy
+};
+
+template <int PV, int DV>
+__device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const Tables &tb, int32_t *W, int m,
+                                        int32_t level, double temp, int64_t x0, int64_t x1, int64_t x2,
+                                        uint8_t *log, int64_t *res, int64_t *trace_row, Regs &R) {
+    const int lane = lane_id();
+    const int32_t N = a.N, B = a.B, RG = a.RG, D = a.D, G = a.G, L = a.L;
+    int64_t Jr = R.Jr, Ar = R.Ar, Ur = R.Ur, s0 = R.s0, s1 = R.s1, s2 = R.s2;
     int64_t b0 = s0, b1 = s1, b2 = s2;
     int32_t best_is_start = 1;
     int32_t *bl = a.best + (int64_t)m * N;
-    const int64_t x0 = a.xscore[0], x1 = a.xscore[1], x2 = a.xscore[2];
     if (lex_less(s0, s1, s2, x0, x1, x2)) {
+        // A start state better than the incumbent is itself a trajectory
+        // best; keep its layout, since the state is updated in place.
         for (int32_t x = lane; x < N; x += kWave) bl[x] = M.cell[x];
         best_is_start = 0;
     }
     int64_t n_acc = 0, n_eval = 0;
     double e_cur = energy(s0, s1, s2, a.scale);
-    uint8_t *log = a.step_log ? a.step_log + (int64_t)m * a.K : nullptr;
     const int half = lane >> 5, hl = lane & 31, cx = lane & 15;
     const bool lay_act = hl < L;  // lane holds layer hl of row-shard a / b
     const bool cell_lane = (lane & 16) == 0;
 
     for (int32_t k0 = 0; k0 < a.K; k0 += kWave) {
         const int32_t k = k0 + lane;
-        const U64x4 b0w = philox4x64_10((uint64_t)k, (uint64_t)(uint32_t)a.level, (uint64_t)(uint32_t)m, 0,
+        const U64x4 b0w = philox4x64_10((uint64_t)k, (uint64_t)(uint32_t)level, (uint64_t)(uint32_t)m, 0,
                                         a.seed, 0);
-        const U64x4 b1w = philox4x64_10((uint64_t)k, (uint64_t)(uint32_t)a.level, (uint64_t)(uint32_t)m, 1,
+        const U64x4 b1w = philox4x64_10((uint64_t)k, (uint64_t)(uint32_t)level, (uint64_t)(uint32_t)m, 1,
                                         a.seed, 0);
         const uint64_t w0 = b0w.v[0], w1 = b0w.v[1], w2 = b0w.v[2], w3 = b0w.v[3];
         const uint64_t w4 = b1w.v[0], w5 = b1w.v[1], w6 = b1w.v[2], w7 = b1w.v[3];
@@ -417,7 +520,7 @@ __global__ void __launch_bounds__(512) k_anneal_chain(AnnealArgs a) {
             const bool reloc = fw0 < a.rho;
             n_eval += 1;
             const int32_t ra = c1 / D, rb = c2 / D;
-            const int32_t ga = s_shard[c1 - ra * D], gb = s_shard[c2 - rb * D];
+            const int32_t ga = tb.shard[c1 - ra * D], gb = tb.shard[c2 - rb * D];
             const int32_t ha = ra * G + ga, hb = rb * G + gb;
             const bool two = ha != hb;
             // W rows of a and b, q rows of i and j: issue the loads first.
@@ -440,12 +543,12 @@ __global__ void __launch_bounds__(512) k_anneal_chain(AnnealArgs a) {
             }
             // cell statistics of the two row-shards (lanes (half, cx))
             const int32_t gsel = half ? gb : ga, rsel = half ? rb : ra;
-            const int32_t cnt = s_count[gsel];
+            const int32_t cnt = tb.count[gsel];
             const bool cact = cell_lane && cx < cnt && (half == 0 || two);
             int64_t Tc = 0, Qc = 0;
             int32_t cc = -1;
             if (cact) {
-                cc = rsel * D + s_slots[gsel * D + cx];
+                cc = rsel * D + tb.slots[gsel * D + cx];
                 Tc = M.T[cc];
                 Qc = M.Q[cc];
                 if (cc == c1) {
@@ -517,7 +620,7 @@ __global__ void __launch_bounds__(512) k_anneal_chain(AnnealArgs a) {
                 if (!(delta > 0.0)) {
                     accept = true;  // z = 0 and exp(0) = 1 > u
                 } else {
-                    const double z = delta / a.temp;
+                    const double z = delta / temp;
                     const double u = (double)fw7 * (1.0 / 4294967296.0);
                     accept = u < exp_det(-z);
                 }
@@ -596,7 +699,7 @@ __global__ void __launch_bounds__(512) k_anneal_chain(AnnealArgs a) {
             }
             {
                 const int64_t incl = row_incl_scan64(cw);
-                if (cact) M.Cp[rsel * D + s_soff[gsel] + cx] = incl;
+                if (cact) M.Cp[rsel * D + tb.soff[gsel] + cx] = incl;
             }
             if (lane == ha) {
                 Jr = Ja;
@@ -626,39 +729,420 @@ __global__ void __launch_bounds__(512) k_anneal_chain(AnnealArgs a) {
             }
         }
     }
-    // ---- epilogue: the terminal state back to the slab
-    wsync();
-    {
-        const int32_t n4 = N >> 2;
-        int4 *c4 = reinterpret_cast<int4 *>(g_cell), *p4 = reinterpret_cast<int4 *>(g_pool);
-        const ushort4 *lc4 = reinterpret_cast<const ushort4 *>(M.cell), *lp4 = reinterpret_cast<const ushort4 *>(M.pool);
-        for (int32_t x = lane; x < n4; x += kWave) {
-            const ushort4 u = lc4[x], v = lp4[x];
-            c4[x] = make_int4(u.x, u.y, u.z, u.w);
-            p4[x] = make_int4(v.x, v.y, v.z, v.w);
-        }
-        for (int32_t x = (n4 << 2) + lane; x < N; x += kWave) {
-            g_cell[x] = M.cell[x];
-            g_pool[x] = M.pool[x];
-        }
-    }
-    for (int32_t x = lane; x <= B; x += kWave) g_start[x] = M.start[x];
-    for (int32_t x = lane; x < B; x += kWave) {
-        g_T[x] = M.T[x];
-        g_Q[x] = M.Q[x];
-    }
-    if (lane < RG) {
-        g_J[lane] = Jr;
-        g_A[lane] = Ar;
-    }
+    R.Jr = Jr;
+    R.Ar = Ar;
+    R.Ur = Ur;
+    R.s0 = s0;
+    R.s1 = s1;
+    R.s2 = s2;
     if (lane == 0) {
-        int64_t *res = a.results + (int64_t)m * kRes;
         res[0] = s0; res[1] = s1; res[2] = s2;
         res[3] = b0; res[4] = b1; res[5] = b2;
         res[6] = n_acc; res[7] = n_eval;
         res[8] = best_is_start;
         res[9] = m;
+        if (trace_row) {
+            trace_row[0] = s0; trace_row[1] = s1; trace_row[2] = s2;
+            trace_row[3] = b0; trace_row[4] = b1; trace_row[5] = b2;
+            trace_row[6] = n_acc; trace_row[7] = n_eval;
+        }
     }
+    return LevelOut{b0, b1, b2, e_cur};
+}
+
+}  // namespace
+
+// One level of every member: state from the member's slab, K proposals,
+// state back to the slab.
+template <int PV, int DV>
+__global__ void __launch_bounds__(512) k_anneal_chain(AnnealArgs a) {
+    extern __shared__ __align__(16) char smem[];
+    const Tables tb = load_tables(a, smem);
+    const int wv = wave_id();
+    const int m = blockIdx.x * a.mpw + wv;
+    if (m >= a.pop) return;  // no block barrier follows
+    const Lds M = member_lds(a, smem, wv);
+    const SlabPtrs g = slab_ptrs(a, a.slabs + (int64_t)a.slab_of[m] * a.off.bytes);
+    Regs R;
+    member_load(a, M, tb, g, R);
+    member_level<PV, DV>(a, M, tb, g.W, m, a.level, a.temp, a.xscore[0], a.xscore[1], a.xscore[2],
+                         a.step_log ? a.step_log + (int64_t)m * a.K : nullptr, a.results + (int64_t)m * kRes,
+                         nullptr, R);
+    member_store(a, M, g, R);
+}
+
+// ---------------------------------------------------------------------------
+// Whole schedule in one cooperative launch.  Every workgroup stays resident;
+// a wave keeps its member's state in LDS and registers from level to level.
+// Wave gw owns slab gw for the whole run; the member it runs changes with
+// resampling.  After a level, every workgroup computes the same level end
+// from the members' result rows: the incumbent update, the systematic
+// resampling parents, and the slab hand-over (the first child of a parent
+// keeps the parent's wave and slab; every further child takes the wave of a
+// member without children, which reloads the parent's published state).
+// Grid barriers: A after the results, B after publishing parent states, C
+// after the copies (only when there are copies).
+
+namespace {
+
+constexpr unsigned kSpinLimit = 1u << 22;
+
+// Grid-wide barrier on a monotonic arrival counter; false if it timed out
+// (then every workgroup stops).  Every thread of the workgroup takes part.
+__device__ inline bool grid_sync(unsigned *bar, unsigned target, int32_t *err, int32_t *s_ok) {
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        __hip_atomic_fetch_add(bar, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        unsigned spins = 0;
+        int32_t good = 1;
+        while (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+            __builtin_amdgcn_s_sleep(2);
+            if (++spins > kSpinLimit || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+                __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                good = 0;
+                break;
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        *s_ok = good;
+    }
+    __syncthreads();
+    return *s_ok != 0;
+}
+
+// Exclusive prefix over the workgroup of one value per thread (thread
+// order); *total gets the sum.  Uses red[0 .. waves).
+__device__ inline uint64_t block_excl_scan(uint64_t v, uint64_t *red, uint64_t *total) {
+    const int lane = lane_id(), wv = wave_id(), nwv = blockDim.x / kWave;
+    const uint64_t incl = wave_incl_scan_u(v);
+    if (lane == kWave - 1) red[wv] = incl;
+    __syncthreads();
+    uint64_t base = 0, tot = 0;
+    for (int w = 0; w < nwv; ++w) {
+        base += w < wv ? red[w] : 0;
+        tot += red[w];
+    }
+    __syncthreads();
+    *total = tot;
+    return base + incl - v;
+}
+
+}  // namespace
+
+
+constexpr int kRunMaxWaves = 4;  // members per workgroup of the whole-schedule kernel
+
+namespace {
+
+template <int CTRL>
+__device__ inline void lexmin_step(int64_t &k0, int64_t &k1, int64_t &k2, int64_t &kj) {
+    const int64_t o0 = dpp64<CTRL>(k0, k0), o1 = dpp64<CTRL>(k1, k1);
+    const int64_t o2 = dpp64<CTRL>(k2, k2), oj = dpp64<CTRL>(kj, kj);
+    if (lex_less(o0, o1, o2, k0, k1, k2) || (o0 == k0 && o1 == k1 && o2 == k2 && oj < kj)) {
+        k0 = o0;
+        k1 = o1;
+        k2 = o2;
+        kj = oj;
+    }
+}
+
+// Lexicographic minimum of (k0, k1, k2) over the wave, lowest kj on ties;
+// the result is uniform.
+__device__ inline void wave_lexmin(int64_t &k0, int64_t &k1, int64_t &k2, int64_t &kj) {
+    lexmin_step<kDppXor1>(k0, k1, k2, kj);
+    lexmin_step<kDppXor2>(k0, k1, k2, kj);
+    lexmin_step<kDppHalfMirror>(k0, k1, k2, kj);
+    lexmin_step<kDppMirror>(k0, k1, k2, kj);
+    int64_t b0 = (int64_t)readlane64((uint64_t)k0, 0), b1 = (int64_t)readlane64((uint64_t)k1, 0);
+    int64_t b2 = (int64_t)readlane64((uint64_t)k2, 0), bj = (int64_t)readlane64((uint64_t)kj, 0);
+#pragma unroll
+    for (int row = 1; row < 4; ++row) {
+        const int64_t o0 = (int64_t)readlane64((uint64_t)k0, 16 * row), o1 = (int64_t)readlane64((uint64_t)k1, 16 * row);
+        const int64_t o2 = (int64_t)readlane64((uint64_t)k2, 16 * row), oj = (int64_t)readlane64((uint64_t)kj, 16 * row);
+        if (lex_less(o0, o1, o2, b0, b1, b2) || (o0 == b0 && o1 == b1 && o2 == b2 && oj < bj)) {
+            b0 = o0;
+            b1 = o1;
+            b2 = o2;
+            bj = oj;
+        }
+    }
+    k0 = b0;
+    k1 = b1;
+    k2 = b2;
+    kj = bj;
+}
+
+template <int CTRL>
+__device__ inline double fmin_step(double v) {
+    const double o = __builtin_bit_cast(double, dpp64<CTRL>(__builtin_bit_cast(int64_t, v), __builtin_bit_cast(int64_t, v)));
+    return o < v ? o : v;
+}
+
+// Minimum of doubles over the wave (no NaN); uniform.
+__device__ inline double wave_min_f64(double v) {
+    v = fmin_step<kDppXor1>(v);
+    v = fmin_step<kDppXor2>(v);
+    v = fmin_step<kDppHalfMirror>(v);
+    v = fmin_step<kDppMirror>(v);
+    double r = __builtin_bit_cast(double, (int64_t)readlane64((uint64_t)__builtin_bit_cast(int64_t, v), 0));
+#pragma unroll
+    for (int row = 1; row < 4; ++row) {
+        const double o = __builtin_bit_cast(double, (int64_t)readlane64((uint64_t)__builtin_bit_cast(int64_t, v), 16 * row));
+        r = o < r ? o : r;
+    }
+    return r;
+}
+
+}  // namespace
+
+template <int PV, int DV>
+__global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(AnnealArgs a, RunArgs r) {
+    extern __shared__ __align__(16) char smem[];
+    __shared__ int64_t s_xs[3], s_k[kRunMaxWaves][4];
+    __shared__ uint64_t s_red[kRunMaxWaves];
+    __shared__ double s_dred[kRunMaxWaves];
+    __shared__ int32_t s_win, s_ok;
+    const Tables tb = load_tables(a, smem);
+    const int tid = threadIdx.x, nt = blockDim.x, lane = lane_id(), wv = wave_id(), nwv = nt / kWave;
+    const int32_t pop = a.pop, N = a.N, K = a.K;
+    const int gw = blockIdx.x * a.mpw + wv;  // this wave's slab
+    const bool active = gw < pop;
+    const int nb = gridDim.x;
+    uint64_t *Fs = reinterpret_cast<uint64_t *>(smem + r.o_lend);
+    int32_t *par = reinterpret_cast<int32_t *>(Fs + pop);
+    int32_t *flag = par + pop;    // has-child flags, then the slab -> next member map
+    int32_t *freed = flag + pop;  // slabs of members without children, ascending member
+    int32_t *slab = freed + pop;  // slab of each member
+    int32_t *slabn = slab + pop;  // slab of each member after the hand-over
+    for (int32_t j = tid; j < pop; j += nt) slab[j] = j;
+    if (tid < 3) s_xs[tid] = r.xscore[tid];
+    __syncthreads();
+    Lds M{};
+    SlabPtrs g{};
+    Regs R{};
+    int m = gw;
+    if (active) {
+        M = member_lds(a, smem, wv);
+        g = slab_ptrs(a, a.slabs + (int64_t)gw * a.off.bytes);
+        member_load(a, M, tb, g, R);
+    }
+    unsigned epoch = 0;
+    const uint64_t P = (uint64_t)pop;
+    const int64_t nW16 = (int64_t)a.RG * a.LP / 4;  // W of a slab in 16-byte units
+    for (int n = 0; n < r.n_sweeps; ++n) {
+        const int32_t level = r.offset + n;
+        const double temp = r.temps[n];
+        // ---- the level, then this workgroup's share of the level end
+        int64_t k0 = LLONG_MAX, k1 = LLONG_MAX, k2 = LLONG_MAX, kj = LLONG_MAX;
+        double emin = __builtin_inf();
+        if (active) {
+            const LevelOut lo = member_level<PV, DV>(
+                a, M, tb, g.W, m, level, temp, s_xs[0], s_xs[1], s_xs[2],
+                r.step_log ? r.step_log + ((int64_t)n * pop + m) * K : nullptr, a.results + (int64_t)m * kRes,
+                r.trace ? r.trace + ((int64_t)n * pop + m) * 8 : nullptr, R);
+            if (lane == 0) r.energy[m] = lo.e;
+            k0 = lo.b0;
+            k1 = lo.b1;
+            k2 = lo.b2;
+            kj = m;
+            emin = lo.e;
+        }
+        if (lane == 0) {
+            s_k[wv][0] = k0; s_k[wv][1] = k1; s_k[wv][2] = k2; s_k[wv][3] = kj;
+            s_dred[wv] = emin;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            for (int w = 1; w < nwv; ++w) {
+                if (lex_less(s_k[w][0], s_k[w][1], s_k[w][2], s_k[0][0], s_k[0][1], s_k[0][2]) ||
+                    (s_k[w][0] == s_k[0][0] && s_k[w][1] == s_k[0][1] && s_k[w][2] == s_k[0][2] &&
+                     s_k[w][3] < s_k[0][3]))
+                    for (int f = 0; f < 4; ++f) s_k[0][f] = s_k[w][f];
+                s_dred[0] = s_dred[w] < s_dred[0] ? s_dred[w] : s_dred[0];
+            }
+            for (int f = 0; f < 4; ++f) r.wg_best[(int64_t)blockIdx.x * 4 + f] = s_k[0][f];
+            r.wg_emin[blockIdx.x] = s_dred[0];
+        }
+        if (!grid_sync(r.bar, (unsigned)nb * ++epoch, r.err, &s_ok)) return;  // A
+
+        // ---- every workgroup: incumbent and minimum energy from the workgroup summaries
+        const double t_next = n + 1 < r.n_sweeps ? r.temps[n + 1] : r.t_after;
+        const bool resample = t_next > 0.0;
+        const int32_t per = (pop + nt - 1) / nt;
+        const int32_t jlo = tid * per < pop ? tid * per : pop, jhi = jlo + per < pop ? jlo + per : pop;
+        {
+            k0 = k1 = k2 = kj = LLONG_MAX;
+            emin = __builtin_inf();
+            for (int b = tid; b < nb; b += nt) {
+                const int64_t *wb = r.wg_best + (int64_t)b * 4;
+                const int64_t v0 = wb[0], v1 = wb[1], v2 = wb[2], vj = wb[3];
+                const double e = r.wg_emin[b];
+                if (lex_less(v0, v1, v2, k0, k1, k2) || (v0 == k0 && v1 == k1 && v2 == k2 && vj < kj)) {
+                    k0 = v0; k1 = v1; k2 = v2; kj = vj;
+                }
+                emin = e < emin ? e : emin;
+            }
+            wave_lexmin(k0, k1, k2, kj);
+            emin = wave_min_f64(emin);
+            if (lane == 0) {
+                s_k[wv][0] = k0; s_k[wv][1] = k1; s_k[wv][2] = k2; s_k[wv][3] = kj;
+                s_dred[wv] = emin;
+            }
+            // the energies of this thread's members (used by the resampling weights)
+            for (int32_t j = jlo; j < jhi; ++j) Fs[j] = __builtin_bit_cast(uint64_t, r.energy[j]);
+            __syncthreads();
+            if (tid == 0) {
+                for (int w = 1; w < nwv; ++w) {
+                    if (lex_less(s_k[w][0], s_k[w][1], s_k[w][2], s_k[0][0], s_k[0][1], s_k[0][2]) ||
+                        (s_k[w][0] == s_k[0][0] && s_k[w][1] == s_k[0][1] && s_k[w][2] == s_k[0][2] &&
+                         s_k[w][3] < s_k[0][3]))
+                        for (int f = 0; f < 4; ++f) s_k[0][f] = s_k[w][f];
+                    s_dred[0] = s_dred[w] < s_dred[0] ? s_dred[w] : s_dred[0];
+                }
+                const bool better = lex_less(s_k[0][0], s_k[0][1], s_k[0][2], s_xs[0], s_xs[1], s_xs[2]);
+                s_win = better ? (int32_t)s_k[0][3] : -1;
+                if (better) {
+                    s_xs[0] = s_k[0][0];
+                    s_xs[1] = s_k[0][1];
+                    s_xs[2] = s_k[0][2];
+                }
+            }
+            __syncthreads();
+        }
+        if (s_win >= 0) {
+            // x* := the winner's trajectory best, one slice per workgroup
+            const int32_t sl = (N + nb - 1) / nb, x0 = blockIdx.x * sl, x1 = x0 + sl < N ? x0 + sl : N;
+            const int32_t *src = a.best + (int64_t)s_win * N;
+            for (int32_t x = x0 + tid; x < x1; x += nt) r.xstar[x] = src[x];
+            if (blockIdx.x == 0 && tid < 3) r.xscore[tid] = s_xs[tid];
+        }
+        // ---- systematic resampling with quantised Boltzmann weights
+        if (resample) {
+            emin = s_dred[0];
+            const double den = fabs(emin) > 1.0 ? fabs(emin) : 1.0;
+            const double cfac = (1.0 / t_next) - (1.0 / temp);
+            uint64_t local = 0;
+            for (int32_t j = jlo; j < jhi; ++j) {
+                const double en = (__builtin_bit_cast(double, Fs[j]) - emin) / den;
+                const uint64_t w = (uint64_t)floor(__builtin_ldexp(exp_det(-(cfac * en)), 40));
+                Fs[j] = w;
+                local += w;
+            }
+            uint64_t total = 0;
+            uint64_t run = block_excl_scan(local, s_red, &total);
+            for (int32_t j = jlo; j < jhi; ++j) {
+                run += Fs[j];
+                Fs[j] = run;
+            }
+            __syncthreads();
+            const U64x4 blk = philox4x64_10(0, (uint64_t)(uint32_t)level, 0xFFFFFFFFull, 2, a.seed, 0);
+            const uint64_t V = blk.v[0] >> 32;
+            for (int32_t mm = tid; mm < pop; mm += nt) {
+                const unsigned __int128 rhs = (unsigned __int128)total * (V + ((uint64_t)mm << 32));
+                int32_t l = 0, h = pop - 1;
+                while (l < h) {
+                    const int32_t md = (l + h) >> 1;
+                    if ((unsigned __int128)Fs[md] * P * ((uint64_t)1 << 32) >= rhs) h = md;
+                    else l = md + 1;
+                }
+                par[mm] = l;
+                flag[mm] = 0;
+            }
+        } else {
+            for (int32_t mm = tid; mm < pop; mm += nt) par[mm] = mm;
+        }
+        __syncthreads();
+        if (r.parents_out) {
+            const int32_t sl = (pop + nb - 1) / nb, p0 = blockIdx.x * sl, p1 = p0 + sl < pop ? p0 + sl : pop;
+            for (int32_t mm = p0 + tid; mm < p1; mm += nt)
+                r.parents_out[(int64_t)n * pop + mm] = resample ? par[mm] : -1;
+        }
+        // ---- slab hand-over
+        int32_t m_next = m, src_slab = -1;
+        if (resample) {
+            for (int32_t mm = tid; mm < pop; mm += nt) flag[par[mm]] = 1;
+            __syncthreads();
+            int32_t n_dead = 0, n_dup = 0;
+            for (int32_t j = jlo; j < jhi; ++j) {
+                n_dead += flag[j] == 0;
+                n_dup += (j > 0 && par[j] == par[j - 1]);
+            }
+            uint64_t tdead = 0, tdup = 0;
+            int32_t rdead = (int32_t)block_excl_scan((uint64_t)n_dead, s_red, &tdead);
+            int32_t rdup = (int32_t)block_excl_scan((uint64_t)n_dup, s_red, &tdup);
+            for (int32_t j = jlo; j < jhi; ++j)
+                if (flag[j] == 0) freed[rdead++] = slab[j];
+            __syncthreads();
+            int32_t *dups = reinterpret_cast<int32_t *>(Fs);  // further children, ascending
+            for (int32_t mm = jlo; mm < jhi; ++mm) {
+                const int32_t pp = par[mm];
+                if (mm == 0 || pp != par[mm - 1]) {
+                    slabn[mm] = slab[pp];
+                } else {
+                    dups[rdup] = mm;
+                    slabn[mm] = freed[rdup++];
+                }
+            }
+            __syncthreads();
+            for (int32_t mm = tid; mm < pop; mm += nt) flag[slabn[mm]] = mm;  // slab -> next member
+            __syncthreads();
+            bool publish = false;
+            if (active) {
+                m_next = flag[gw];
+                const int32_t pn = par[m_next];
+                if (m_next > 0 && par[m_next - 1] == pn) src_slab = slab[pn];
+                // the current member publishes its state when it has a second child
+                int32_t l = 0, h = pop;
+                while (l < h) {
+                    const int32_t md = (l + h) >> 1;
+                    if (par[md] < m) l = md + 1;
+                    else h = md;
+                }
+                publish = l + 1 < pop && par[l] == m && par[l + 1] == m;
+            }
+            // Every further child gets its parent's W in its own slab; the
+            // copies are split evenly over all workgroups.
+            {
+                const int32_t *dups = reinterpret_cast<const int32_t *>(Fs);
+                const int64_t units = (int64_t)tdup * nW16;
+                const int64_t share = (units + nb - 1) / nb;
+                const int64_t u0 = (int64_t)blockIdx.x * share, u1 = u0 + share < units ? u0 + share : units;
+                constexpr int U = 4;
+                for (int64_t base = u0; base < u1; base += U * nt) {
+                    int4 v[U];
+                    int4 *dst[U];
+#pragma unroll
+                    for (int u = 0; u < U; ++u) {
+                        const int64_t x = base + u * nt + tid;
+                        dst[u] = nullptr;
+                        if (x < u1) {
+                            const int32_t c = dups[x / nW16];
+                            const int64_t off = x - (x / nW16) * nW16;
+                            v[u] = reinterpret_cast<const int4 *>(a.slabs + (int64_t)slab[par[c]] * a.off.bytes + a.off.W)[off];
+                            dst[u] = reinterpret_cast<int4 *>(a.slabs + (int64_t)slabn[c] * a.off.bytes + a.off.W) + off;
+                        }
+                    }
+#pragma unroll
+                    for (int u = 0; u < U; ++u)
+                        if (dst[u]) *dst[u] = v[u];
+                }
+            }
+            // and the rest of its state from the parent's own slab
+            if (publish) member_store(a, M, g, R);
+        }
+        if (!grid_sync(r.bar, (unsigned)nb * ++epoch, r.err, &s_ok)) return;  // B
+        if (resample) {
+            if (active && src_slab >= 0)
+                member_load(a, M, tb, slab_ptrs(a, a.slabs + (int64_t)src_slab * a.off.bytes), R);
+            for (int32_t mm = tid; mm < pop; mm += nt) slab[mm] = slabn[mm];
+            __syncthreads();
+        }
+        m = m_next;
+    }
+    if (active) member_store(a, M, g, R);
+    if (blockIdx.x == 0)
+        for (int32_t mm = tid; mm < pop; mm += nt) r.slab_of_out[mm] = slab[mm];
 }
 
 // Launch shape of the chain kernel; false when the problem is outside its
@@ -706,6 +1190,54 @@ static int chain_launch_t(const AnnealArgs &a, hipStream_t stream) {
     const unsigned grid = (unsigned)((a.pop + a.mpw - 1) / a.mpw);
     hipLaunchKernelGGL((k_anneal_chain<PV, DV>), dim3(grid), dim3(kWave * a.mpw), lds, stream, a);
     return hipGetLastError() == hipSuccess ? ROUTEPACK_OK : ROUTEPACK_E_DEVICE;
+}
+
+// Level-end tables of the whole-schedule kernel (after the member regions).
+static int64_t run_lend_bytes(int32_t pop) { return 28 * (int64_t)pop; }
+
+template <int PV, int DV>
+static int chain_run_t(const AnnealArgs &a, const RunArgs &r0, int32_t n_cu, bool launch, hipStream_t stream) {
+    RunArgs r = r0;
+    if (a.mpw > kRunMaxWaves) return ROUTEPACK_E_UNSUPPORTED;
+    const int64_t o_lend = ((int64_t)a.lds_shared + (int64_t)a.mpw * a.lds_member + 15) & ~(int64_t)15;
+    const int64_t lds = o_lend + run_lend_bytes(a.pop);
+    // static LDS of the kernel is below 1 KiB
+    if (lds + 1024 > 160 * 1024) return ROUTEPACK_E_UNSUPPORTED;
+    r.o_lend = (int32_t)o_lend;
+    const void *fn = (const void *)k_anneal_chain_run<PV, DV>;
+    if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+        return ROUTEPACK_E_DEVICE;
+    const int grid = (a.pop + a.mpw - 1) / a.mpw, block = kWave * a.mpw;
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, block, (size_t)lds) != hipSuccess)
+        return ROUTEPACK_E_DEVICE;
+    if ((int64_t)per_cu * n_cu < grid) return ROUTEPACK_E_UNSUPPORTED;  // not all resident
+    if (!launch) return ROUTEPACK_OK;
+    AnnealArgs aa = a;
+    void *args[] = {&aa, &r};
+    if (hipLaunchCooperativeKernel(fn, dim3(grid), dim3(block), args, (unsigned)lds, stream) != hipSuccess)
+        return ROUTEPACK_E_DEVICE;
+    return hipGetLastError() == hipSuccess ? ROUTEPACK_OK : ROUTEPACK_E_DEVICE;
+}
+
+// Checks (launch = false) or launches (launch = true) the whole-schedule
+// kernel; ROUTEPACK_E_UNSUPPORTED when its workgroups cannot all be resident.
+int chain_run(const AnnealArgs &a, const RunArgs &r, int32_t pv, int32_t dv, int32_t n_cu, bool launch,
+              hipStream_t stream) {
+    if (dv == 8) {
+        switch (pv) {
+            case 4: return chain_run_t<4, 8>(a, r, n_cu, launch, stream);
+            case 8: return chain_run_t<8, 8>(a, r, n_cu, launch, stream);
+            case 16: return chain_run_t<16, 8>(a, r, n_cu, launch, stream);
+        }
+    } else {
+        switch (pv) {
+            case 4: return chain_run_t<4, 16>(a, r, n_cu, launch, stream);
+            case 8: return chain_run_t<8, 16>(a, r, n_cu, launch, stream);
+            case 16: return chain_run_t<16, 16>(a, r, n_cu, launch, stream);
+        }
+    }
+    return ROUTEPACK_E_UNSUPPORTED;
 }
 
 int launch_anneal_chain(const AnnealArgs &a, int32_t pv, int32_t dv, hipStream_t stream) {

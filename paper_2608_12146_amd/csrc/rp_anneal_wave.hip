@@ -662,14 +662,28 @@ __global__ void __launch_bounds__(512) k_anneal_wave(AnnealArgs a) {
 }
 
 // Copies the slab of each duplicated parent into the slab its extra child
-// takes over (entries 0 .. n_copies-1 of src/dst).
+// takes over (entries 0 .. n_copies-1 of src/dst).  Each copy is split over
+// kCopySplit workgroups, four 16-byte loads in flight per thread.
+constexpr int kCopySplit = 8;
 __global__ void __launch_bounds__(256) k_copy_slabs(char *slabs, int64_t bytes, const int32_t *src,
                                                     const int32_t *dst, const int32_t *n_copies) {
-    const int b = blockIdx.x;
+    const int b = blockIdx.x / kCopySplit, part = blockIdx.x % kCopySplit;
     if (b >= *n_copies) return;
+    const int64_t n16 = bytes / 16;
+    const int64_t per = (n16 + kCopySplit - 1) / kCopySplit;
+    const int64_t lo = part * per, hi = lo + per < n16 ? lo + per : n16;
     const int4 *s = reinterpret_cast<const int4 *>(slabs + (int64_t)src[b] * bytes);
     int4 *d = reinterpret_cast<int4 *>(slabs + (int64_t)dst[b] * bytes);
-    for (int64_t x = threadIdx.x; x < bytes / 16; x += blockDim.x) d[x] = s[x];
+    const int64_t step = blockDim.x;
+    int64_t x = lo + threadIdx.x;
+    for (; x + 3 * step < hi; x += 4 * step) {
+        const int4 v0 = s[x], v1 = s[x + step], v2 = s[x + 2 * step], v3 = s[x + 3 * step];
+        d[x] = v0;
+        d[x + step] = v1;
+        d[x + 2 * step] = v2;
+        d[x + 3 * step] = v3;
+    }
+    for (; x < hi; x += step) d[x] = s[x];
 }
 
 // Chooses the wave kernel's launch shape; returns false when a member's
@@ -726,7 +740,8 @@ int launch_anneal_wave(const AnnealArgs &a, bool tlds, hipStream_t stream) {
 
 int launch_copy_slabs(char *slabs, int64_t bytes, const int32_t *src, const int32_t *dst,
                       const int32_t *n_copies, int32_t pop, hipStream_t stream) {
-    hipLaunchKernelGGL(k_copy_slabs, dim3(pop), dim3(256), 0, stream, slabs, bytes, src, dst, n_copies);
+    hipLaunchKernelGGL(k_copy_slabs, dim3(pop * kCopySplit), dim3(256), 0, stream, slabs, bytes, src, dst,
+                       n_copies);
     return hipGetLastError() == hipSuccess ? ROUTEPACK_OK : ROUTEPACK_E_DEVICE;
 }
 

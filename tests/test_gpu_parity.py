@@ -112,7 +112,7 @@ def _compare_anneal(g, o, steps=False):
         assert np.array_equal(g["steps"].cpu().numpy(), o["steps"])
 
 
-KERNELS = ["chain", "wave", "workgroup"]
+KERNELS = ["chain_run", "chain", "wave", "workgroup"]
 
 
 def _use_kernel(monkeypatch, kernel):
@@ -141,7 +141,7 @@ def test_anneal_full_trajectory_tiny(G, kernel, monkeypatch):
     _compare_anneal(g, o, steps=True)
 
 
-# The chain kernel holds one row-shard per lane (R* G <= 64 row-shards).
+# The chain kernels hold one row-shard per lane (R* G <= 64 row-shards).
 CHAIN_MAX_ROW_SHARDS = 64
 
 
@@ -156,8 +156,8 @@ def test_anneal_small_levels(G, kernel, monkeypatch):
     pr = _packed("small", G)
     temps = synth.anneal_temperatures(w.levels)[:40]
     K = synth.windows.STEPS_PER_LEVEL
-    if kernel == "chain" and pr["r_star"] * G > CHAIN_MAX_ROW_SHARDS:
-        _log(f"anneal small G={G}: {pr['r_star'] * G} row-shards, chain kernel refuses")
+    if kernel.startswith("chain") and pr["r_star"] * G > CHAIN_MAX_ROW_SHARDS:
+        _log(f"anneal small G={G}: {pr['r_star'] * G} row-shards, {kernel} kernel refuses")
         with pytest.raises(rp.RoutepackError) as ei:
             rp.anneal(rp.Problem.from_dict(pd), w.lengths, q, pr["r_star"], pr["population"], temps[:1], K,
                       w.seed_anneal)
@@ -186,7 +186,7 @@ def _mid_oracle_levels():
 
 
 @gpu
-@pytest.mark.parametrize("kernel", ["chain", "wave"])
+@pytest.mark.parametrize("kernel", ["chain_run", "chain", "wave"])
 def test_anneal_mid_sampled_levels(kernel, monkeypatch):
     """Mid window at its full population: two levels from the seeds, then one
     late level resumed from the GPU's population, each checked against the
