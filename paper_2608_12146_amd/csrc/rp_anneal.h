@@ -47,6 +47,8 @@ struct AnnealArgs {
     int32_t lds_shared, lds_member;
     int32_t o_cell, o_pool, o_start, o_T, o_Q, o_acost, o_Jpre;
     int32_t o_Jpiv, o_tshared;  // chain kernel: J pivots (per member), lengths table (shared)
+    uint32_t ginv, dinv;        // chain kernel: ceil(2^32 / G), ceil(2^32 / D) (unused when G, D == 1)
+    int32_t dv, o_hcnt, o_hcell;  // chain kernel: cost-prefix stride; row-shard slot tables (shared)
     unsigned long long *phase_cycles;  // [pop][8] with RP_PHASE_TIMERS builds, else unused
 };
 

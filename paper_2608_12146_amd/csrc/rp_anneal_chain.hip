@@ -47,11 +47,26 @@ __device__ inline int64_t row_incl_scan64(int64_t v) {
 struct Lds {
     uint16_t *cell, *pool, *start;
     int32_t *T;
-    int64_t *Q, *Cp, *Jpre, *Jpiv;
+    int64_t *Q;
+    int64_t *Cp;    // [RG][DV] prefix of the cell costs of each row-shard, slot order; kInf past its slots
+    int64_t *Ctot;  // [RG] total cell cost of each row-shard
+    int64_t *Jpre, *Vpre;  // [64] prefixes of the source and target roulette weights (kInf past RG)
+    int64_t *Jpiv, *Vpiv;  // [8] their entries 8k+7
 };
+
+// floor(w m / 2^64) without a branch on the size of m (m varies by lane).
+__device__ inline uint64_t bounded_lane(uint64_t w, uint64_t m) { return __umul64hi(w, m); }
+
+// floor(x / d) for 0 <= x < 2^16 and 1 <= d < 2^16, with inv = ceil(2^32 / d)
+// (exact: x d < 2^32); d == 1 is passed through.
+__device__ inline int32_t div_small(int32_t x, int32_t d, uint32_t inv) {
+    return d == 1 ? x : (int32_t)__umulhi((uint32_t)x, inv);
+}
 
 struct Tables {
     const int32_t *slots, *count, *shard, *soff, *t;
+    const int32_t *hcnt;   // [RG] slots of each row-shard
+    const int32_t *hcell;  // [RG][DV] cell of each slot of each row-shard
 };
 
 // Screen result of one proposal (per lane).
@@ -71,63 +86,65 @@ __device__ inline Screen screen(const AnnealArgs &a, const Lds &M, const Tables 
     const int32_t N = a.N, B = a.B, RG = a.RG, D = a.D, G = a.G;
     const bool guided = (uint32_t)w0 < a.p_guide;
     const bool reloc = (uint32_t)(w0 >> 32) < a.rho;
-    // Uniform-mode indices (used by lanes whose proposal is not guided).
+    // Uniform-mode proposal: samples (and the target cell of a relocation)
+    // straight from the words; its reads go out first.
     const int32_t ir = (int32_t)bounded(w1, (uint64_t)N);
     const int32_t jr = (int32_t)bounded(w4, (uint64_t)N);
-    const int32_t cir = M.cell[ir], cjr = M.cell[jr];
+    const int32_t cir = clamp0(M.cell[ir], B - 1), cjr = clamp0(M.cell[jr], B - 1);
     const int32_t tir = tb.t[ir], tjr = tb.t[jr];
     int32_t c1 = cir, c2 = reloc ? (int32_t)bounded(w4, (uint64_t)B) : cjr;
+    int32_t T1 = M.T[c1], T2 = M.T[c2];
+    int32_t sz1 = (int32_t)M.start[c1 + 1] - (int32_t)M.start[c1];
     int32_t i = ir, j = reloc ? -1 : jr;
     int32_t ti = tir, tj = reloc ? 0 : tjr;
     sc.pos_i = -1;
     sc.pos_j = -1;
     if (__ballot(guided)) {
-        // Source row-shard: roulette over J; target: over s2 - J_h + 1.
+        // Source row-shard: roulette over J; target: over s2 - J_h + 1, whose
+        // prefix is V_h = (h + 1)(s2 + 1) - J_pre[h].  Both prefixes are
+        // non-decreasing: count the pivots, then the entries of one block.
         const uint64_t pk1 = bounded(w1, (uint64_t)s1);
-        const int64_t sp1 = s2 + 1;
-        const uint64_t pk4 = bounded(w4, (uint64_t)((int64_t)RG * sp1 - s1));
+        const uint64_t pk4 = bounded(w4, (uint64_t)((int64_t)RG * (s2 + 1) - s1));
         int32_t k1 = 0, k4 = 0;
 #pragma unroll
         for (int k = 0; k < 8; ++k) {
-            const int64_t pv = M.Jpiv[k];
-            k1 += (uint64_t)pv <= pk1 ? 1 : 0;
-            k4 += (pv != kInf && (uint64_t)((int64_t)(8 * k + 8) * sp1 - pv) <= pk4) ? 1 : 0;
+            k1 += (uint64_t)M.Jpiv[k] <= pk1 ? 1 : 0;
+            k4 += (uint64_t)M.Vpiv[k] <= pk4 ? 1 : 0;
         }
         int32_t h1 = 8 * k1, h4 = 8 * k4;
-        const int64_t *f1 = M.Jpre + 8 * k1, *f4 = M.Jpre + 8 * k4;
+        const int64_t *f1 = M.Jpre + 8 * k1, *f4 = M.Vpre + 8 * k4;
 #pragma unroll
         for (int x = 0; x < 8; ++x) {
-            const int64_t v1 = f1[x], v4 = f4[x];
-            h1 += (uint64_t)v1 <= pk1 ? 1 : 0;
-            h4 += (v4 != kInf && (uint64_t)((int64_t)(8 * k4 + x + 1) * sp1 - v4) <= pk4) ? 1 : 0;
+            h1 += (uint64_t)f1[x] <= pk1 ? 1 : 0;
+            h4 += (uint64_t)f4[x] <= pk4 ? 1 : 0;
         }
         if (s1 == 0) h1 = (int32_t)bounded(w1, (uint64_t)RG);
         h1 = clamp0(h1, RG - 1);
         h4 = clamp0(h4, RG - 1);
-        const int32_t r1 = h1 / G, g1 = h1 - r1 * G, r2 = h4 / G, g2 = h4 - r2 * G;
-        const int32_t cnt1 = tb.count[g1], cnt2 = tb.count[g2];
-        const int64_t *cp = M.Cp + r1 * D + tb.soff[g1];
+        // Source cell: roulette over the row-shard's cell costs (prefix padded
+        // with kInf past its slots); target cell: uniform over its slots.
+        const int64_t *cp = M.Cp + h1 * DV;
         int64_t cv[DV];
 #pragma unroll
         for (int x = 0; x < DV; ++x) cv[x] = cp[x];
-        int64_t tot = 0;
-#pragma unroll
-        for (int x = 0; x < DV; ++x) tot = (x == cnt1 - 1) ? cv[x] : tot;
+        const int64_t tot = M.Ctot[h1];
+        const int32_t cnt1 = tb.hcnt[h1], cnt2 = tb.hcnt[h4];
         int32_t xi;
         if (tot == 0) {
             xi = (int32_t)bounded(w2, (uint64_t)cnt1);
         } else {
-            const uint64_t pk2 = bounded(w2, (uint64_t)tot);
+            const uint64_t pk2 = bounded_lane(w2, (uint64_t)tot);
             xi = 0;
 #pragma unroll
-            for (int x = 0; x < DV; ++x) xi += (x < cnt1 && (uint64_t)cv[x] <= pk2) ? 1 : 0;
+            for (int x = 0; x < DV; ++x) xi += (uint64_t)cv[x] <= pk2 ? 1 : 0;
         }
         xi = clamp0(xi, cnt1 - 1);
         const int32_t x2 = (int32_t)bounded(w5, (uint64_t)cnt2);
-        const int32_t gc1 = clamp0(r1 * D + (G == 1 ? xi : tb.slots[g1 * D + xi]), B - 1);
-        const int32_t gc2 = clamp0(r2 * D + (G == 1 ? x2 : tb.slots[g2 * D + x2]), B - 1);
+        const int32_t gc1 = clamp0(G == 1 ? h1 * D + xi : tb.hcell[h1 * DV + xi], B - 1);
+        const int32_t gc2 = clamp0(G == 1 ? h4 * D + x2 : tb.hcell[h4 * DV + x2], B - 1);
         const int32_t st1 = M.start[gc1], en1 = M.start[gc1 + 1];
         const int32_t st2 = M.start[gc2], en2 = M.start[gc2 + 1];
+        const int32_t gT1 = M.T[gc1], gT2 = M.T[gc2];
         const int32_t pi = clamp0(st1 + (int32_t)bounded(w3, (uint64_t)(en1 - st1)), N - 1);
         const int32_t pj = clamp0(st2 + (int32_t)bounded(w6, (uint64_t)(en2 - st2)), N - 1);
         const int32_t gi = M.pool[pi], gj = M.pool[pj];
@@ -135,6 +152,9 @@ __device__ inline Screen screen(const AnnealArgs &a, const Lds &M, const Tables 
         if (guided) {
             c1 = gc1;
             c2 = gc2;
+            T1 = gT1;
+            T2 = gT2;
+            sz1 = en1 - st1;
             i = gi;
             ti = gti;
             sc.pos_i = pi;
@@ -145,10 +165,6 @@ __device__ inline Screen screen(const AnnealArgs &a, const Lds &M, const Tables 
             }
         }
     }
-    c1 = clamp0(c1, B - 1);
-    c2 = clamp0(c2, B - 1);
-    const int32_t T1 = M.T[c1], T2 = M.T[c2];
-    const int32_t sz1 = (int32_t)M.start[c1 + 1] - (int32_t)M.start[c1];
     bool f = c1 != c2;
     if (f) {
         if (!reloc) f = ((int64_t)T1 - ti + tj <= a.C) && ((int64_t)T2 - tj + ti <= a.C);
@@ -262,14 +278,20 @@ __device__ inline void start_add(uint16_t *start16, int32_t lo, int32_t hi, int3
     }
 }
 
-// J prefix over row-shards (lane h holds J_h) into LDS, with the pivot
-// entries J_pre[8k+7]; entries at h >= RG hold kInf.
-__device__ inline void write_jpre(const Lds &M, int64_t Jr, int32_t RG) {
+// Prefixes of the roulette weights into LDS (lane h holds J_h): J_pre and
+// V_h = (h + 1)(s2 + 1) - J_pre[h], with their pivot entries 8k+7; entries at
+// h >= RG hold kInf.
+__device__ inline void write_jpre(const Lds &M, int64_t Jr, int32_t RG, int64_t s2) {
     const int lane = lane_id();
     const int64_t incl = wave_incl_scan(lane < RG ? Jr : 0);
     const int64_t v = lane < RG ? incl : kInf;
+    const int64_t t = lane < RG ? (int64_t)(lane + 1) * (s2 + 1) - incl : kInf;
     M.Jpre[lane] = v;
-    if ((lane & 7) == 7) M.Jpiv[lane >> 3] = v;
+    M.Vpre[lane] = t;
+    if ((lane & 7) == 7) {
+        M.Jpiv[lane >> 3] = v;
+        M.Vpiv[lane >> 3] = t;
+    }
 }
 
 // Member state kept in registers between proposals: J and A of the
@@ -299,7 +321,8 @@ __device__ inline SlabPtrs slab_ptrs(const AnnealArgs &a, char *slab) {
 }
 
 // Workgroup tables in LDS: the slot list, slot count and first cost-prefix
-// index of every EDP shard, the shard of every slot, and the lengths.
+// index of every EDP shard, the shard of every slot, the slot count and slot
+// cells of every row-shard, and the lengths.
 // Every thread of the workgroup takes part (ends with a block barrier).
 __device__ inline Tables load_tables(const AnnealArgs &a, char *smem) {
     const int32_t N = a.N, D = a.D, G = a.G;
@@ -318,12 +341,20 @@ __device__ inline Tables load_tables(const AnnealArgs &a, char *smem) {
             acc += a.count[g];
         }
     }
+    const int32_t RG = a.RG, DVr = a.dv;
+    int32_t *s_hcnt = reinterpret_cast<int32_t *>(smem + a.o_hcnt);
+    int32_t *s_hcell = reinterpret_cast<int32_t *>(smem + a.o_hcell);
+    for (int32_t x = threadIdx.x; x < RG * DVr; x += blockDim.x) {
+        const int32_t h = x / DVr, k = x - h * DVr, r = h / G, g = h - r * G, cnt = a.count[g];
+        if (k == 0) s_hcnt[h] = cnt;
+        s_hcell[x] = r * D + a.slots[g * D + (k < cnt ? k : cnt - 1)];
+    }
     const int32_t n4 = N >> 2;
     const int4 *t4 = reinterpret_cast<const int4 *>(a.t);
     for (int32_t x = threadIdx.x; x < n4; x += blockDim.x) reinterpret_cast<int4 *>(s_t)[x] = t4[x];
     for (int32_t x = (n4 << 2) + threadIdx.x; x < N; x += blockDim.x) s_t[x] = a.t[x];
     __syncthreads();
-    return Tables{s_slots, s_count, s_shard, s_soff, s_t};
+    return Tables{s_slots, s_count, s_shard, s_soff, s_t, s_hcnt, s_hcell};    return Tables{s_slots, s_count, s_shard, s_soff, s_t};
 }
 
 __device__ inline Lds member_lds(const AnnealArgs &a, char *smem, int wv) {
@@ -335,8 +366,11 @@ __device__ inline Lds member_lds(const AnnealArgs &a, char *smem, int wv) {
     M.T = reinterpret_cast<int32_t *>(mine + a.o_T);
     M.Q = reinterpret_cast<int64_t *>(mine + a.o_Q);
     M.Cp = reinterpret_cast<int64_t *>(mine + a.o_acost);
+    M.Ctot = M.Cp + a.RG * a.dv;
     M.Jpre = reinterpret_cast<int64_t *>(mine + a.o_Jpre);
-    M.Jpiv = reinterpret_cast<int64_t *>(mine + a.o_Jpiv);
+    M.Vpre = M.Jpre + 64;
+    M.Jpiv = M.Jpre + 128;
+    M.Vpiv = M.Jpre + 136;
     return M;
 }
 
@@ -346,7 +380,7 @@ __device__ inline Lds member_lds(const AnnealArgs &a, char *smem, int wv) {
 __device__ inline void member_load(const AnnealArgs &a, const Lds &M, const Tables &tb, const SlabPtrs &g,
                                    Regs &R) {
     const int lane = lane_id();
-    const int32_t N = a.N, B = a.B, RG = a.RG, D = a.D, G = a.G;
+    const int32_t N = a.N, B = a.B, RG = a.RG, G = a.G;
     constexpr int U = 16;
     {
         const int32_t n4 = N >> 2;
@@ -403,15 +437,20 @@ __device__ inline void member_load(const AnnealArgs &a, const Lds &M, const Tabl
     wsync();
     // cost prefix of each row-shard's cells, in slot order (lanes over row-shards)
     if (lane < RG) {
-        const int32_t r = lane / G, gg = lane - (lane / G) * G;
+        const int32_t cnt = tb.hcnt[lane];
         int64_t acc = 0;
-        int64_t *cp = M.Cp + r * D + tb.soff[gg];
-        for (int32_t x = 0; x < tb.count[gg]; ++x) {
-            const int32_t c = r * D + tb.slots[gg * D + x];
-            const int64_t t = M.T[c], q = M.Q[c];
-            for (int s = 0; s < a.S; ++s) acc += a.alpha[s] * t + a.beta[s] * q;
-            cp[x] = acc;
+        int64_t *cp = M.Cp + lane * a.dv;
+        for (int32_t x = 0; x < a.dv; ++x) {
+            if (x < cnt) {
+                const int32_t c = tb.hcell[lane * a.dv + x];
+                const int64_t t = M.T[c], q = M.Q[c];
+                for (int s = 0; s < a.S; ++s) acc += a.alpha[s] * t + a.beta[s] * q;
+                cp[x] = acc;
+            } else {
+                cp[x] = kInf;
+            }
         }
+        M.Ctot[lane] = acc;
     }
     // U_g = sum over rows of J(r, g); lane g holds it
     int64_t Ur = 0;
@@ -424,7 +463,7 @@ __device__ inline void member_load(const AnnealArgs &a, const Lds &M, const Tabl
     R.s0 = wave_max(lane < G ? Ur : LLONG_MIN);
     R.s1 = wave_sum(lane < G ? Ur : 0);
     R.s2 = wave_max(lane < RG ? R.Jr : LLONG_MIN);
-    write_jpre(M, R.Jr, RG);
+    write_jpre(M, R.Jr, RG, R.s2);
     wsync();
 }
 
@@ -519,8 +558,8 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
             const uint32_t fw7 = __builtin_amdgcn_readlane((int32_t)(uint32_t)(w7 >> 32), f);
             const bool reloc = fw0 < a.rho;
             n_eval += 1;
-            const int32_t ra = c1 / D, rb = c2 / D;
-            const int32_t ga = tb.shard[c1 - ra * D], gb = tb.shard[c2 - rb * D];
+            const int32_t ra = div_small(c1, D, a.dinv), rb = div_small(c2, D, a.dinv);
+            const int32_t ga = G == 1 ? 0 : tb.shard[c1 - ra * D], gb = G == 1 ? 0 : tb.shard[c2 - rb * D];
             const int32_t ha = ra * G + ga, hb = rb * G + gb;
             const bool two = ha != hb;
             // W rows of a and b, q rows of i and j: issue the loads first.
@@ -542,13 +581,13 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                 }
             }
             // cell statistics of the two row-shards (lanes (half, cx))
-            const int32_t gsel = half ? gb : ga, rsel = half ? rb : ra;
-            const int32_t cnt = tb.count[gsel];
+            const int32_t hsel = half ? hb : ha;
+            const int32_t cnt = tb.hcnt[hsel];
             const bool cact = cell_lane && cx < cnt && (half == 0 || two);
             int64_t Tc = 0, Qc = 0;
             int32_t cc = -1;
             if (cact) {
-                cc = rsel * D + tb.slots[gsel * D + cx];
+                cc = G == 1 ? hsel * D + cx : tb.hcell[hsel * DV + cx];
                 Tc = M.T[cc];
                 Qc = M.Q[cc];
                 if (cc == c1) {
@@ -699,7 +738,8 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
             }
             {
                 const int64_t incl = row_incl_scan64(cw);
-                if (cact) M.Cp[rsel * D + tb.soff[gsel] + cx] = incl;
+                if (cact) M.Cp[hsel * DV + cx] = incl;
+                if (cact && cx == cnt - 1) M.Ctot[hsel] = incl;
             }
             if (lane == ha) {
                 Jr = Ja;
@@ -708,7 +748,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                 Jr = Jb;
                 Ar = Ab;
             }
-            write_jpre(M, Jr, RG);
+            write_jpre(M, Jr, RG, n2);
             Ur = Un;
             s0 = n0;
             s1 = n1;
@@ -1161,11 +1201,16 @@ bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out,
     a.o_start = (int32_t)o; o = up16(o + 2 * up8e((int64_t)a.B + 1));
     a.o_T = (int32_t)o; o = up16(o + 4 * (int64_t)a.B);
     a.o_Q = (int32_t)o; o = up16(o + 8 * (int64_t)a.B);
-    a.o_acost = (int32_t)o; o = up16(o + 8 * ((int64_t)a.B + dv));
-    a.o_Jpre = (int32_t)o; o = up16(o + 8 * 64);
-    a.o_Jpiv = (int32_t)o; o = up16(o + 8 * 8);
+    a.dv = dv;
+    a.o_acost = (int32_t)o; o = up16(o + 8 * ((int64_t)a.RG * dv + a.RG));  // cost prefixes and totals
+    a.o_Jpre = (int32_t)o; o = up16(o + 8 * (64 + 64 + 8 + 8));  // J_pre, V_pre and their pivots
+    a.o_Jpiv = a.o_Jpre + 8 * 128;
+    a.ginv = (uint32_t)((((uint64_t)1 << 32) + (uint64_t)a.G - 1) / (uint64_t)a.G);
+    a.dinv = (uint32_t)((((uint64_t)1 << 32) + (uint64_t)a.D - 1) / (uint64_t)a.D);
     const int64_t member = o;
-    const int64_t tab = up16(4 * ((int64_t)a.G * a.D + 2 * a.G + a.D));
+    int64_t tab = up16(4 * ((int64_t)a.G * a.D + 2 * a.G + a.D));
+    a.o_hcnt = (int32_t)tab; tab = up16(tab + 4 * (int64_t)a.RG);
+    a.o_hcell = (int32_t)tab; tab = up16(tab + 4 * (int64_t)a.RG * dv);
     a.o_tshared = (int32_t)tab;
     const int64_t shared = up16(tab + 4 * (int64_t)a.N);
     const int64_t lim = 160 * 1024;
