@@ -996,6 +996,11 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
     while ((1 << a.pshift) < P) ++a.pshift;
     a.C = prob->capacity;
     a.scale = ldexp((double)prob->capacity, prob->frac_bits);
+    {
+        int e2 = 0;
+        a.scale_pow2 = frexp(a.scale, &e2) == 0.5 ? 1 : 0;
+        a.inv_scale = a.scale_pow2 ? ldexp(1.0, 1 - e2) : 0.0;
+    }
     for (int s = 0; s < prob->n_stages; ++s) {
         a.alpha[s] = prob->alpha_fp[s];
         a.beta[s] = prob->beta_fp[s];

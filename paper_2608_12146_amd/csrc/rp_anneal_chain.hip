@@ -54,6 +54,16 @@ struct Lds {
     int64_t *Jpiv, *Vpiv;  // [8] their entries 8k+7
 };
 
+// Energy of a score (Eq. pa-energy); when the scale 2^F C is a power of two
+// the three quotients are exact products with its reciprocal (identical
+// results, no division).
+__device__ inline double energy_k(const AnnealArgs &a, int64_t s0, int64_t s1, int64_t s2) {
+    if (!a.scale_pow2) return energy(s0, s1, s2, a.scale);
+    const double e0 = (double)s0 * a.inv_scale, e1 = (double)s1 * a.inv_scale, e2 = (double)s2 * a.inv_scale;
+    const double x = e0 + 1e-6 * e1;
+    return x + 1e-9 * e2;
+}
+
 // floor(w m / 2^64) without a branch on the size of m (m varies by lane).
 __device__ inline uint64_t bounded_lane(uint64_t w, uint64_t m) { return __umul64hi(w, m); }
 
@@ -521,7 +531,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
         best_is_start = 0;
     }
     int64_t n_acc = 0, n_eval = 0;
-    double e_cur = energy(s0, s1, s2, a.scale);
+    double e_cur = energy_k(a, s0, s1, s2);
     const int half = lane >> 5, hl = lane & 31, cx = lane & 15;
     const bool lay_act = hl < L;  // lane holds layer hl of row-shard a / b
     const bool cell_lane = (lane & 16) == 0;
@@ -579,6 +589,20 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
 #pragma unroll
                     for (int x = 0; x < PV / 4; ++x) qb[x] = make_int4(0, 0, 0, 0);
                 }
+            }
+            // Commit inputs, read now so they overlap the row loads: the member
+            // ranges of both cells and, when both fit 32 lanes, their members
+            // (half 0: c1, half 1: c2).
+            const int32_t st1 = M.start[c1], en1 = M.start[c1 + 1];
+            const int32_t st2 = M.start[c2], en2 = M.start[c2 + 1];
+            const int32_t sz1 = en1 - st1, sz2 = en2 - st2;
+            const bool small = sz1 <= 32 && sz2 <= 32;
+            int32_t y = -1;
+            bool yv = false;
+            if (small) {
+                const int32_t sz = half ? sz2 : sz1;
+                yv = hl < sz;
+                if (yv) y = M.pool[(half ? st2 : st1) + hl];
             }
             // cell statistics of the two row-shards (lanes (half, cx))
             const int32_t hsel = half ? hb : ha;
@@ -647,11 +671,31 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
             } else {
                 if (lane == ga) Un += dJa;
                 if (lane == gb && two) Un += dJb;
-                n0 = wave_max(lane < G ? Un : LLONG_MIN);
+                // the maximum of the other shards is s0 unless ga or gb held it
+                const int64_t Uga = (int64_t)readlane64((uint64_t)Ur, ga), Ugb = (int64_t)readlane64((uint64_t)Ur, gb);
+                if (Uga < s0 && Ugb < s0) {
+                    if (gb == ga) {
+                        const int64_t na = Uga + dJa + dJb;
+                        n0 = s0 > na ? s0 : na;
+                    } else {
+                        const int64_t na = Uga + dJa, nb = Ugb + dJb;
+                        n0 = s0 > na ? s0 : na;
+                        n0 = n0 > nb ? n0 : nb;
+                    }
+                } else {
+                    n0 = wave_max(lane < G ? Un : LLONG_MIN);
+                }
             }
             const int64_t Jn = lane == ha ? Ja : (lane == hb ? Jb : Jr);
-            const int64_t n2 = wave_max(lane < RG ? Jn : LLONG_MIN);
-            const double e_new = energy(n0, n1, n2, a.scale);
+            // the maximum of the other row-shards is s2 unless ha or hb held it
+            int64_t n2;
+            if (Jha < s2 && Jhb < s2) {
+                n2 = s2 > Ja ? s2 : Ja;
+                n2 = n2 > Jb ? n2 : Jb;
+            } else {
+                n2 = wave_max(lane < RG ? Jn : LLONG_MIN);
+            }
+            const double e_new = energy_k(a, n0, n1, n2);
             bool accept = lex_less(n0, n1, n2, s0, s1, s2);
             if (!accept) {
                 const double den = fabs(e_cur) > 1.0 ? fabs(e_cur) : 1.0;
@@ -671,18 +715,6 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
             if (log && lane == f) log[k] = 2;
             n_acc += 1;
             // ---- commit
-            const int32_t st1 = M.start[c1], en1 = M.start[c1 + 1];
-            const int32_t st2 = M.start[c2], en2 = M.start[c2 + 1];
-            const int32_t sz1 = en1 - st1, sz2 = en2 - st2;
-            // members of both cells, half 0: c1, half 1: c2 (when both fit 32 lanes)
-            const bool small = sz1 <= 32 && sz2 <= 32;
-            int32_t y = -1;
-            bool yv = false;
-            if (small) {
-                const int32_t sz = half ? sz2 : sz1;
-                yv = hl < sz;
-                if (yv) y = M.pool[(half ? st2 : st1) + hl];
-            }
             wsync();
             if (two && lay_act) {
                 int4 *wp = reinterpret_cast<int4 *>(W + ((int64_t)(half ? hb : ha) * L + hl) * PV);
