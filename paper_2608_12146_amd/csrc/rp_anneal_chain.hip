@@ -883,6 +883,43 @@ __device__ inline bool grid_sync(unsigned *bar, unsigned target, int32_t *err, i
     return *s_ok != 0;
 }
 
+// Systematic-resampling parent of a child: the first j with
+// F_j P 2^32 >= rhs (F non-decreasing, the predicate holds at n - 1).  The
+// search gallops from j0 in the direction the predicate asks, then bisects
+// the bracket; near-uniform weights put the answer next to j0.
+__device__ inline int32_t parent_search(const uint64_t *F, int32_t n, uint64_t P, unsigned __int128 rhs, int32_t j0) {
+    auto ok = [&](int32_t j) { return (unsigned __int128)F[j] * P * ((uint64_t)1 << 32) >= rhs; };
+    int32_t lo, hi;  // ok(hi) holds; ok(lo) fails (lo = -1: none known)
+    if (ok(j0)) {
+        hi = j0;
+        lo = -1;
+        for (int32_t step = 1; hi > 0; step <<= 1) {
+            const int32_t c = hi - step < 0 ? 0 : hi - step;
+            if (!ok(c)) {
+                lo = c;
+                break;
+            }
+            hi = c;
+        }
+    } else {
+        lo = j0;
+        hi = n - 1;
+        for (int32_t step = 1; lo + step < n - 1; step <<= 1) {
+            if (ok(lo + step)) {
+                hi = lo + step;
+                break;
+            }
+            lo += step;
+        }
+    }
+    while (hi - lo > 1) {
+        const int32_t md = lo + ((hi - lo) >> 1);
+        if (ok(md)) hi = md;
+        else lo = md;
+    }
+    return hi;
+}
+
 // Exclusive prefix over the workgroup of one value per thread (thread
 // order); *total gets the sum.  Uses red[0 .. waves).
 __device__ inline uint64_t block_excl_scan(uint64_t v, uint64_t *red, uint64_t *total) {
@@ -1110,17 +1147,14 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
             __syncthreads();
             const U64x4 blk = philox4x64_10(0, (uint64_t)(uint32_t)level, 0xFFFFFFFFull, 2, a.seed, 0);
             const uint64_t V = blk.v[0] >> 32;
-            for (int32_t mm = tid; mm < pop; mm += nt) {
+            // children of this thread: [jlo, jhi); parents are non-decreasing
+            int32_t pj = jlo < pop ? jlo : pop - 1;
+            for (int32_t mm = jlo; mm < jhi; ++mm) {
                 const unsigned __int128 rhs = (unsigned __int128)total * (V + ((uint64_t)mm << 32));
-                int32_t l = 0, h = pop - 1;
-                while (l < h) {
-                    const int32_t md = (l + h) >> 1;
-                    if ((unsigned __int128)Fs[md] * P * ((uint64_t)1 << 32) >= rhs) h = md;
-                    else l = md + 1;
-                }
-                par[mm] = l;
-                flag[mm] = 0;
+                pj = parent_search(Fs, pop, P, rhs, pj);
+                par[mm] = pj;
             }
+            for (int32_t mm = tid; mm < pop; mm += nt) flag[mm] = 0;
         } else {
             for (int32_t mm = tid; mm < pop; mm += nt) par[mm] = mm;
         }
@@ -1133,18 +1167,22 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
         // ---- slab hand-over
         int32_t m_next = m, src_slab = -1;
         if (resample) {
-            for (int32_t mm = tid; mm < pop; mm += nt) flag[par[mm]] = 1;
+            // bit 0: the member has a child; bit 1: a second one
+            for (int32_t mm = tid; mm < pop; mm += nt)
+                atomicOr(&flag[par[mm]], (mm > 0 && par[mm - 1] == par[mm]) ? 3 : 1);
             __syncthreads();
+            // the current member publishes its state when it has a second child
+            const bool publish = active && (flag[m] & 2) != 0;
             int32_t n_dead = 0, n_dup = 0;
             for (int32_t j = jlo; j < jhi; ++j) {
-                n_dead += flag[j] == 0;
+                n_dead += (flag[j] & 1) == 0;
                 n_dup += (j > 0 && par[j] == par[j - 1]);
             }
             uint64_t tdead = 0, tdup = 0;
             int32_t rdead = (int32_t)block_excl_scan((uint64_t)n_dead, s_red, &tdead);
             int32_t rdup = (int32_t)block_excl_scan((uint64_t)n_dup, s_red, &tdup);
             for (int32_t j = jlo; j < jhi; ++j)
-                if (flag[j] == 0) freed[rdead++] = slab[j];
+                if ((flag[j] & 1) == 0) freed[rdead++] = slab[j];
             __syncthreads();
             int32_t *dups = reinterpret_cast<int32_t *>(Fs);  // further children, ascending
             for (int32_t mm = jlo; mm < jhi; ++mm) {
@@ -1159,19 +1197,10 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
             __syncthreads();
             for (int32_t mm = tid; mm < pop; mm += nt) flag[slabn[mm]] = mm;  // slab -> next member
             __syncthreads();
-            bool publish = false;
             if (active) {
                 m_next = flag[gw];
                 const int32_t pn = par[m_next];
                 if (m_next > 0 && par[m_next - 1] == pn) src_slab = slab[pn];
-                // the current member publishes its state when it has a second child
-                int32_t l = 0, h = pop;
-                while (l < h) {
-                    const int32_t md = (l + h) >> 1;
-                    if (par[md] < m) l = md + 1;
-                    else h = md;
-                }
-                publish = l + 1 < pop && par[l] == m && par[l + 1] == m;
             }
             // Every further child gets its parent's W in its own slab; the
             // copies are split evenly over all workgroups.
