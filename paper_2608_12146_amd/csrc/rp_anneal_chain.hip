@@ -945,44 +945,6 @@ constexpr int kRunMaxWaves = 4;  // members per workgroup of the whole-schedule 
 namespace {
 
 template <int CTRL>
-__device__ inline void lexmin_step(int64_t &k0, int64_t &k1, int64_t &k2, int64_t &kj) {
-    const int64_t o0 = dpp64<CTRL>(k0, k0), o1 = dpp64<CTRL>(k1, k1);
-    const int64_t o2 = dpp64<CTRL>(k2, k2), oj = dpp64<CTRL>(kj, kj);
-    if (lex_less(o0, o1, o2, k0, k1, k2) || (o0 == k0 && o1 == k1 && o2 == k2 && oj < kj)) {
-        k0 = o0;
-        k1 = o1;
-        k2 = o2;
-        kj = oj;
-    }
-}
-
-// Lexicographic minimum of (k0, k1, k2) over the wave, lowest kj on ties;
-// the result is uniform.
-__device__ inline void wave_lexmin(int64_t &k0, int64_t &k1, int64_t &k2, int64_t &kj) {
-    lexmin_step<kDppXor1>(k0, k1, k2, kj);
-    lexmin_step<kDppXor2>(k0, k1, k2, kj);
-    lexmin_step<kDppHalfMirror>(k0, k1, k2, kj);
-    lexmin_step<kDppMirror>(k0, k1, k2, kj);
-    int64_t b0 = (int64_t)readlane64((uint64_t)k0, 0), b1 = (int64_t)readlane64((uint64_t)k1, 0);
-    int64_t b2 = (int64_t)readlane64((uint64_t)k2, 0), bj = (int64_t)readlane64((uint64_t)kj, 0);
-#pragma unroll
-    for (int row = 1; row < 4; ++row) {
-        const int64_t o0 = (int64_t)readlane64((uint64_t)k0, 16 * row), o1 = (int64_t)readlane64((uint64_t)k1, 16 * row);
-        const int64_t o2 = (int64_t)readlane64((uint64_t)k2, 16 * row), oj = (int64_t)readlane64((uint64_t)kj, 16 * row);
-        if (lex_less(o0, o1, o2, b0, b1, b2) || (o0 == b0 && o1 == b1 && o2 == b2 && oj < bj)) {
-            b0 = o0;
-            b1 = o1;
-            b2 = o2;
-            bj = oj;
-        }
-    }
-    k0 = b0;
-    k1 = b1;
-    k2 = b2;
-    kj = bj;
-}
-
-template <int CTRL>
 __device__ inline double fmin_step(double v) {
     const double o = __builtin_bit_cast(double, dpp64<CTRL>(__builtin_bit_cast(int64_t, v), __builtin_bit_cast(int64_t, v)));
     return o < v ? o : v;

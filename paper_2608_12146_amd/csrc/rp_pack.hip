@@ -20,6 +20,7 @@
 //                  successful trial; drop canonical duplicates (first kept);
 //                  order by (score, discovery); fill the population cyclically.
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <vector>
@@ -362,6 +363,363 @@ __global__ void __launch_bounds__(64) k_pack_trials(TrialArgs a) {
     if (lane == 0) a.ok[b] = 1;
 }
 
+// ---------------------------------------------------------------------------
+// Seed trials in three launches for the common shapes (C < 2^32, N and K
+// below 2^16, the trial's W table within LDS); the single-kernel path above
+// covers the rest.  Same draws, same decisions.
+//
+//  k_pack_fit      one wave per candidate: WindowShuffle and
+//                  RandomizedBestFit with the draws, window items and their
+//                  lengths prefetched 64 steps ahead into lane registers; the
+//                  ranked pick compares 64-bit keys (load, then fewer
+//                  members, then lower index) with DPP maxima.  Ends with the
+//                  member list of every cell.
+//  k_pack_cellsum  one workgroup per (candidate, cell): Q_k = sum of the
+//                  member rows and peak_k = sum_l max_p Q_k.
+//  k_pack_pair     one workgroup per candidate: EDPAwarePair with the W table
+//                  in LDS, threads over 4 consecutive entries of W + Q_k and a
+//                  DPP maximum over each layer's ranks, and the next cell's Q
+//                  row prefetched during each step.
+
+struct PackFast {
+    int32_t *mstart;  // [M-1][K+1] member list offsets
+    int32_t *mlist;   // [M-1][N] members, grouped by cell
+};
+
+// RandomizedBestFit key of a cell: a larger key comes first.
+__device__ inline uint64_t fit_key(int64_t T, int32_t n, int32_t c) {
+    return ((uint64_t)T << 32) | ((uint64_t)(0xFFFF - n) << 16) | (uint64_t)(0xFFFF - c);
+}
+
+__global__ void __launch_bounds__(64) k_pack_fit(TrialArgs a, PackFast pf) {
+    extern __shared__ int64_t sfit[];
+    const int lane = lane_id();
+    const int b = blockIdx.x;
+    const int32_t N = a.N, K = a.K;
+    int64_t *sT = sfit;
+    int32_t *sN = reinterpret_cast<int32_t *>(sT + K);
+    int32_t *cur = sN + K;
+    int32_t *cellk = a.cellk + (int64_t)b * N;
+    for (int32_t c = lane; c < K; c += kWave) {
+        sT[c] = 0;
+        sN[c] = 0;
+    }
+    __syncthreads();
+    int32_t good = 1;
+    if (b == 0) {
+        for (int32_t i = lane; i < N; i += kWave) {
+            const int32_t c = a.x_length[i];
+            cellk[i] = c;
+            atomicAdd(&sN[c], 1);
+        }
+    } else {
+        const int32_t w = a.w;
+        const uint64_t *wd = a.words + (int64_t)(b - 1) * (2 * (int64_t)N + K);
+        // window: lane x < wsize holds item x and its length
+        int32_t win = -1, wint = 0;
+        if (lane < w && lane < N) {
+            win = a.sigma[lane];
+            wint = a.t[win];
+        }
+        int32_t next = w < N ? w : N, wsize = next;
+        // prefetched sigma items entering the window, with their lengths
+        int32_t sbase = next;
+        int32_t sreg = sbase + lane < N ? a.sigma[sbase + lane] : 0;
+        int32_t streg = sbase + lane < N ? a.t[sreg] : 0;
+        // prefetched draws: shuffle word h and best-fit word h
+        int32_t hbase = 0;
+        uint64_t wr1 = lane < N ? wd[lane] : 0, wr2 = lane < N ? wd[N + lane] : 0;
+        for (int32_t h = 0; h < N; ++h) {
+            if (h - hbase == kWave) {
+                hbase += kWave;
+                wr1 = hbase + lane < N ? wd[hbase + lane] : 0;
+                wr2 = hbase + lane < N ? wd[N + hbase + lane] : 0;
+            }
+            const int32_t pos = (int32_t)bounded(readlane64(wr1, h - hbase), (uint64_t)wsize);
+            const int32_t item = __builtin_amdgcn_readlane(win, pos);
+            const int64_t ti = __builtin_amdgcn_readlane(wint, pos);
+            // remove position pos, append the next sigma item
+            const int32_t up = __shfl_down(win, 1, kWave), upt = __shfl_down(wint, 1, kWave);
+            if (lane >= pos && lane < wsize - 1) {
+                win = up;
+                wint = upt;
+            }
+            if (next < N) {
+                if (next - sbase == kWave) {
+                    sbase += kWave;
+                    sreg = sbase + lane < N ? a.sigma[sbase + lane] : 0;
+                    streg = sbase + lane < N ? a.t[sreg] : 0;
+                }
+                const int32_t ni = __builtin_amdgcn_readlane(sreg, next - sbase);
+                const int32_t nt = __builtin_amdgcn_readlane(streg, next - sbase);
+                if (lane == wsize - 1) {
+                    win = ni;
+                    wint = nt;
+                }
+                ++next;
+            } else {
+                if (lane == wsize - 1) {
+                    win = -1;
+                    wint = 0;
+                }
+                --wsize;
+            }
+            int32_t c;
+            if (h < K) {
+                c = h;
+            } else {
+                uint64_t best = 0;
+                int32_t nf = 0;
+                for (int32_t cb = 0; cb < K; cb += kWave) {
+                    const int32_t cc = cb + lane;
+                    const bool f = cc < K && sT[cc] + ti <= a.C;
+                    nf += __popcll(__ballot(f));
+                    if (f) {
+                        const uint64_t k = fit_key(sT[cc], sN[cc], cc);
+                        best = k > best ? k : best;
+                    }
+                }
+                if (nf == 0) {
+                    good = 0;
+                    break;
+                }
+                best = wave_max_u64(best);
+                const int32_t wp = w < nf ? w : nf;
+                const int32_t rho = (int32_t)bounded(readlane64(wr2, h - hbase), (uint64_t)wp);
+                for (int32_t pass = 1; pass <= rho; ++pass) {
+                    const uint64_t prev = best;
+                    best = 0;
+                    for (int32_t cb = 0; cb < K; cb += kWave) {
+                        const int32_t cc = cb + lane;
+                        if (cc < K && sT[cc] + ti <= a.C) {
+                            const uint64_t k = fit_key(sT[cc], sN[cc], cc);
+                            if (k < prev && k > best) best = k;
+                        }
+                    }
+                    best = wave_max_u64(best);
+                }
+                c = 0xFFFF - (int32_t)(best & 0xFFFF);
+            }
+            if (lane == 0) {
+                sT[c] += ti;
+                sN[c] += 1;
+                cellk[item] = c;
+            }
+            __syncthreads();
+        }
+    }
+    if (lane == 0) a.ok[b] = good;
+    if (!good) return;
+    __syncthreads();
+    // member lists: offsets by an exclusive scan of the counts, then a scatter
+    int32_t *ms = pf.mstart + (int64_t)b * (K + 1);
+    int32_t *ml = pf.mlist + (int64_t)b * N;
+    int64_t carry = 0;
+    for (int32_t cb = 0; cb < K; cb += kWave) {
+        const int32_t cc = cb + lane;
+        const int64_t v = cc < K ? sN[cc] : 0;
+        const int64_t incl = wave_incl_scan(v);
+        if (cc < K) {
+            ms[cc] = (int32_t)(carry + incl - v);
+            cur[cc] = (int32_t)(carry + incl - v);
+        }
+        carry += (int64_t)readlane64((uint64_t)incl, kWave - 1);
+    }
+    if (lane == 0) ms[K] = N;
+    __syncthreads();
+    for (int32_t i = lane; i < N; i += kWave) {
+        const int32_t c = cellk[i];
+        ml[atomicAdd(&cur[c], 1)] = i;
+    }
+}
+
+// Q_k and peak_k of cell k = blockIdx.x of candidate b = blockIdx.y.
+__global__ void __launch_bounds__(128) k_pack_cellsum(TrialArgs a, PackFast pf) {
+    extern __shared__ int32_t sq[];
+    __shared__ int64_t spart[4];
+    const int b = blockIdx.y, k = blockIdx.x, tid = threadIdx.x, nt = blockDim.x;
+    if (!a.ok[b]) return;  // uniform: a failed trial has no layout
+    const int32_t K = a.K, LP = a.LP, L = a.L, P = a.P;
+    const int32_t *ms = pf.mstart + (int64_t)b * (K + 1);
+    const int32_t *ml = pf.mlist + (int64_t)b * a.N;
+    const int32_t lo = ms[k], hi = ms[k + 1];
+    int32_t *Qk = a.Qc + ((int64_t)b * K + k) * LP;
+    for (int32_t e = tid; e < LP; e += nt) {
+        int32_t acc = 0;
+        for (int32_t x = lo; x < hi; ++x) acc += a.q[(int64_t)ml[x] * LP + e];
+        Qk[e] = acc;
+        sq[e] = acc;
+    }
+    __syncthreads();
+    int64_t part = 0;
+    for (int32_t l = tid; l < L; l += nt) {
+        int32_t mx = sq[l * P];
+        for (int32_t p = 1; p < P; ++p) mx = max(mx, sq[l * P + p]);
+        part += mx;
+    }
+    part = wave_sum(part);
+    if (lane_id() == 0) spart[wave_id()] = part;
+    __syncthreads();
+    if (tid == 0) {
+        int64_t tot = 0;
+        for (int w = 0; w < nt / kWave; ++w) tot += spart[w];
+        a.peak[(int64_t)b * K + k] = tot;
+    }
+}
+
+// EDPAwarePair of candidate b (block per candidate).
+__global__ void __launch_bounds__(256) k_pack_pair(TrialArgs a, PackFast pf) {
+    extern __shared__ __align__(16) char spair[];
+    __shared__ int32_t s_h;
+    const int b = blockIdx.x, tid = threadIdx.x, nt = blockDim.x, lane = lane_id(), wv = wave_id();
+    if (!a.ok[b]) return;  // uniform
+    const int32_t N = a.N, K = a.K, RG = a.RG, LP = a.LP, L = a.L, P = a.P, G = a.G, D = a.D;
+    const int32_t w = b == 0 ? 1 : a.w;
+    const uint64_t *wd = b == 0 ? nullptr : a.words + (int64_t)(b - 1) * (2 * (int64_t)N + K);
+    int64_t *after = reinterpret_cast<int64_t *>(spair);            // [RG]
+    int64_t *pkv = after + RG, *base = pkv + RG;                    // [RG], [RG]
+    int64_t *speak = base + RG;                                     // [K]
+    int32_t *Wl = reinterpret_cast<int32_t *>(speak + K + ((3 * RG + K) & 1));  // [RG][LP], 16-byte aligned
+    int32_t *qb = Wl + (int64_t)RG * LP;                            // [2][LP]
+    int32_t *mxs = qb + 2 * LP;                                     // [RG][L]
+    int32_t *filled = mxs + RG * L;                                 // [RG]
+    int32_t *hcnt = filled + RG;                                    // [RG]
+    int32_t *order = hcnt + RG;                                     // [K]
+    int32_t *cell_to = order + K;                                   // [K]
+    const int32_t *Qc = a.Qc + (int64_t)b * K * LP;
+    for (int32_t k = tid; k < K; k += nt) speak[k] = a.peak[(int64_t)b * K + k];
+    for (int64_t x = tid; x < (int64_t)RG * LP; x += nt) Wl[x] = 0;
+    for (int32_t h = tid; h < RG; h += nt) {
+        base[h] = 0;
+        filled[h] = 0;
+        hcnt[h] = a.count[h % G];
+    }
+    __syncthreads();
+    // order: cells by decreasing peak, then index
+    for (int32_t k = tid; k < K; k += nt) {
+        const int64_t v = speak[k];
+        int32_t rank = 0;
+        for (int32_t f = 0; f < K; ++f) {
+            const int64_t u = speak[f];
+            rank += (u > v) || (u == v && f < k);
+        }
+        order[rank] = k;
+    }
+    __syncthreads();
+    for (int32_t e = tid; e < LP; e += nt) qb[e] = Qc[(int64_t)order[0] * LP + e];
+    __syncthreads();
+    constexpr int kPre = 16;  // Q entries per thread held for the next step (LP <= 16 * 256)
+    for (int32_t pos = 0; pos < K; ++pos) {
+        const int32_t k = order[pos];
+        const int32_t *qk = qb + (pos & 1) * LP;
+        // next cell's Q row into registers while this step runs
+        int32_t nq[kPre];
+        const bool more = pos + 1 < K;
+        const int64_t nrow = more ? (int64_t)order[pos + 1] * LP : 0;
+#pragma unroll
+        for (int u = 0; u < kPre; ++u) {
+            const int32_t e = tid + u * nt;
+            nq[u] = more && e < LP ? Qc[nrow + e] : 0;
+        }
+        // per (row-shard, layer): max over ranks of W + Q_k; a thread holds 4
+        // consecutive entries, a layer's ranks span P / 4 adjacent threads.
+        // Every thread runs the same number of iterations, so the DPP maximum
+        // always sees its whole group.
+        {
+            const int32_t c4 = LP >> 2, g4 = P >> 2;
+            const int32_t iters = (RG * c4 + nt - 1) / nt;
+            int32_t y = tid, h = 0;
+            while (y >= c4) {
+                y -= c4;
+                ++h;
+            }
+            for (int32_t it = 0; it < iters; ++it) {
+                const bool cand = h < RG && filled[h] < hcnt[h];
+                int32_t mx = INT32_MIN;
+                if (cand) {
+                    const int4 wv4 = reinterpret_cast<const int4 *>(Wl + (int64_t)h * LP)[y];
+                    const int4 qv4 = reinterpret_cast<const int4 *>(qk)[y];
+                    mx = max(max(wv4.x + qv4.x, wv4.y + qv4.y), max(wv4.z + qv4.z, wv4.w + qv4.w));
+                }
+                mx = seg_max32(mx, g4);
+                if (cand && (y & (g4 - 1)) == 0) mxs[h * L + y / g4] = mx;
+                y += nt;
+                while (y >= c4) {
+                    y -= c4;
+                    ++h;
+                }
+            }
+        }
+        __syncthreads();
+        for (int32_t h = tid; h < RG; h += nt) {
+            int64_t af = 0, pk = 0;
+            if (filled[h] < hcnt[h]) {
+                for (int32_t l = 0; l < L; ++l) {
+                    const int32_t mx = mxs[h * L + l];
+                    af += mx;
+                    pk = mx > pk ? mx : pk;
+                }
+            }
+            after[h] = af;
+            pkv[h] = pk;
+        }
+        __syncthreads();
+        if (wv == 0) {
+            // candidates in EDPAwarePair order (increase, peak, index); the
+            // rho-th of the leading min(w, |candidates|)
+            int32_t cnt = 0;
+            for (int32_t hb = 0; hb < RG; hb += kWave)
+                cnt += __popcll(__ballot(hb + lane < RG && filled[hb + lane] < hcnt[hb + lane]));
+            const int32_t wp = w < cnt ? w : cnt;
+            int32_t rho = 0;
+            if (wp > 1) {
+                const uint64_t total = (((uint64_t)1) << wp) - 1;
+                const uint64_t pick = bounded(wd[2 * (int64_t)N + pos], total);
+                uint64_t pref = 0;
+                for (rho = 0; rho < wp; ++rho) {
+                    pref += ((uint64_t)1) << (wp - 1 - rho);
+                    if (pref > pick) break;
+                }
+            }
+            int64_t p0 = LLONG_MIN, p1 = LLONG_MIN, p2 = LLONG_MIN;
+            for (int32_t pass = 0; pass <= rho; ++pass) {
+                int64_t k0 = LLONG_MAX, k1 = LLONG_MAX, k2 = LLONG_MAX, kj = LLONG_MAX;
+                for (int32_t hb = 0; hb < RG; hb += kWave) {
+                    const int32_t h = hb + lane;
+                    if (h < RG && filled[h] < hcnt[h]) {
+                        const int64_t v0 = after[h] - base[h], v1 = pkv[h], v2 = h;
+                        if ((pass == 0 || lex_less(p0, p1, p2, v0, v1, v2)) && lex_less(v0, v1, v2, k0, k1, k2)) {
+                            k0 = v0; k1 = v1; k2 = v2; kj = v2;
+                        }
+                    }
+                }
+                wave_lexmin(k0, k1, k2, kj);
+                p0 = k0; p1 = k1; p2 = k2;
+            }
+            if (lane == 0) s_h = (int32_t)p2;
+        }
+        __syncthreads();
+        const int32_t h = s_h;
+        for (int32_t e = tid; e < LP; e += nt) Wl[(int64_t)h * LP + e] += qk[e];
+        if (tid == 0) {
+            const int32_t r = h / G, g = h - r * G;
+            base[h] = after[h];
+            cell_to[k] = r * D + a.slots[g * D + filled[h]];
+            filled[h] += 1;
+        }
+        int32_t *qn = qb + ((pos + 1) & 1) * LP;
+#pragma unroll
+        for (int u = 0; u < kPre; ++u) {
+            const int32_t e = tid + u * nt;
+            if (more && e < LP) qn[e] = nq[u];
+        }
+        __syncthreads();
+    }
+    const int32_t *cellk = a.cellk + (int64_t)b * N;
+    int32_t *out = a.out + (int64_t)b * N;
+    for (int32_t i = tid; i < N; i += nt) out[i] = cell_to[cellk[i]];
+}
+
 // Canonical form of layouts[b] (b < n) into canon[b].
 __global__ void __launch_bounds__(256) k_canonical(const int32_t *layouts, int32_t n, int32_t N, int32_t R,
                                                    int32_t D, int32_t G, const int32_t *slots,
@@ -581,7 +939,28 @@ extern "C" int routepack_pack_rows(const routepack_problem *prob, const int32_t 
     hipLaunchKernelGGL(k_fill_i32, dim3(256), dim3(256), 0, stream, cand, (int64_t)M * N, 0);
     hipLaunchKernelGGL(k_fill_i32, dim3(1), dim3(64), 0, stream, okv, (int64_t)M, 0);
     RP_HIP(hipMemcpyAsync(cand, x_len, sizeof(int32_t) * N, hipMemcpyDeviceToDevice, stream));
-    hipLaunchKernelGGL(k_pack_trials, dim3(nb), dim3(64), 0, stream, ta);
+    // Seed trials: three kernels for the common shapes, else one.
+    // ROUTEPACK_PACK_KERNEL=single requests the single-kernel path.
+    const char *pk_force = getenv("ROUTEPACK_PACK_KERNEL");
+    const int64_t pair_lds = 8 * (3 * (int64_t)RG + K + 1) +
+                             4 * ((int64_t)RG * LP + 2 * LP + (int64_t)RG * prob->n_layers + 2 * (int64_t)RG + 2 * (int64_t)K);
+    const bool fast = !(pk_force && strcmp(pk_force, "single") == 0) && C < ((int64_t)1 << 31) && N < 65536 &&
+                      prob->n_ranks >= 4 && LP > 0 && pair_lds <= 150 * 1024;
+    if (fast) {
+        PackFast pf;
+        pf.mstart = scr.get<int32_t>((size_t)nb * (K + 1));
+        pf.mlist = scr.get<int32_t>((size_t)nb * N);
+        if (scr.failed()) return ROUTEPACK_E_DEVICE;
+        const size_t fit_lds = (size_t)16 * K;
+        RP_HIP(hipFuncSetAttribute((const void *)k_pack_fit, hipFuncAttributeMaxDynamicSharedMemorySize, (int)fit_lds));
+        RP_HIP(hipFuncSetAttribute((const void *)k_pack_pair, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                   (int)pair_lds));
+        hipLaunchKernelGGL(k_pack_fit, dim3(nb), dim3(64), fit_lds, stream, ta, pf);
+        hipLaunchKernelGGL(k_pack_cellsum, dim3(K, nb), dim3(128), (size_t)4 * LP, stream, ta, pf);
+        hipLaunchKernelGGL(k_pack_pair, dim3(nb), dim3(256), (size_t)pair_lds, stream, ta, pf);
+    } else {
+        hipLaunchKernelGGL(k_pack_trials, dim3(nb), dim3(64), 0, stream, ta);
+    }
     RP_HIP(hipGetLastError());
     // Score every candidate (failed trials leave garbage layouts: their
     // status is nonzero or they are ignored by the selection).

@@ -251,9 +251,17 @@ def test_anneal_crowded_cells(G, kernel, monkeypatch):
 @gpu
 @pytest.mark.parametrize("name,G", [("tiny", 1), ("tiny", 2), ("small", 1), ("small", 4),
                                     ("mid", 1), ("mid", 2)])
-def test_pack_rows(name, G):
+@pytest.mark.parametrize("path", ["default", "single"])
+def test_pack_rows(name, G, path, monkeypatch):
+    """Row count and seed population equal to the oracle's; "single" requests
+    the one-kernel seed trials, "default" the library's choice (three
+    kernels where the shape allows)."""
     rp = _rp()
-    _log(f"pack_rows {name} G={G}")
+    if path == "single":
+        monkeypatch.setenv("ROUTEPACK_PACK_KERNEL", "single")
+    else:
+        monkeypatch.delenv("ROUTEPACK_PACK_KERNEL", raising=False)
+    _log(f"pack_rows {name} G={G} ({path} seed trials)")
     w, pd, pb, agg, slot, load, q = _window(name, G)
     pr = _packed(name, G)
     g = rp.pack_rows(rp.Problem.from_dict(pd), w.lengths, q, w.seed_pack, synth.windows.N_TRIALS,
