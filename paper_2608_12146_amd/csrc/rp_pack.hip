@@ -439,7 +439,14 @@ __global__ void __launch_bounds__(64) k_pack_fit(TrialArgs a, PackFast pf) {
             const int32_t item = __builtin_amdgcn_readlane(win, pos);
             const int64_t ti = __builtin_amdgcn_readlane(wint, pos);
             // remove position pos, append the next sigma item
-            const int32_t up = __shfl_down(win, 1, kWave), upt = __shfl_down(wint, 1, kWave);
+            int32_t up, upt;
+            if (w <= 16) {  // row_shl:1 -- lane i reads lane i + 1 of its 16-lane row
+                up = __builtin_amdgcn_update_dpp(win, win, 0x101, 0xF, 0xF, false);
+                upt = __builtin_amdgcn_update_dpp(wint, wint, 0x101, 0xF, 0xF, false);
+            } else {
+                up = __shfl_down(win, 1, kWave);
+                upt = __shfl_down(wint, 1, kWave);
+            }
             if (lane >= pos && lane < wsize - 1) {
                 win = up;
                 wint = upt;
@@ -533,6 +540,158 @@ __global__ void __launch_bounds__(64) k_pack_fit(TrialArgs a, PackFast pf) {
     }
 }
 
+// k_pack_fit for K <= 64 NCH cells: lane x holds the load, member count and
+// key of cells x, x + 64, ... in registers, so the ranked passes need no LDS
+// traffic and a placement updates one lane.
+template <int NCH>
+__global__ void __launch_bounds__(64) k_pack_fit_reg(TrialArgs a, PackFast pf) {
+    extern __shared__ int32_t sfitr[];  // [K] counts, then [K] cursors
+    const int lane = lane_id();
+    const int b = blockIdx.x;
+    const int32_t N = a.N, K = a.K;
+    int32_t *cnt_s = sfitr, *cur = sfitr + K;
+    int32_t *cellk = a.cellk + (int64_t)b * N;
+    int64_t Tr[NCH];
+    int32_t nr[NCH];
+    uint64_t kr[NCH];
+#pragma unroll
+    for (int u = 0; u < NCH; ++u) {
+        const int32_t c = u * kWave + lane;
+        Tr[u] = 0;
+        nr[u] = 0;
+        kr[u] = c < K ? fit_key(0, 0, c) : 0;
+    }
+    int32_t good = 1;
+    if (b == 0) {
+        for (int32_t c = lane; c < K; c += kWave) cnt_s[c] = 0;
+        __syncthreads();
+        for (int32_t i = lane; i < N; i += kWave) {
+            const int32_t c = a.x_length[i];
+            cellk[i] = c;
+            atomicAdd(&cnt_s[c], 1);
+        }
+    } else {
+        const int32_t w = a.w;
+        const uint64_t *wd = a.words + (int64_t)(b - 1) * (2 * (int64_t)N + K);
+        int32_t win = -1, wint = 0;
+        if (lane < w && lane < N) {
+            win = a.sigma[lane];
+            wint = a.t[win];
+        }
+        int32_t next = w < N ? w : N, wsize = next;
+        int32_t sbase = next;
+        int32_t sreg = sbase + lane < N ? a.sigma[sbase + lane] : 0;
+        int32_t streg = sbase + lane < N ? a.t[sreg] : 0;
+        int32_t hbase = 0;
+        uint64_t wr1 = lane < N ? wd[lane] : 0, wr2 = lane < N ? wd[N + lane] : 0;
+        for (int32_t h = 0; h < N; ++h) {
+            if (h - hbase == kWave) {
+                hbase += kWave;
+                wr1 = hbase + lane < N ? wd[hbase + lane] : 0;
+                wr2 = hbase + lane < N ? wd[N + hbase + lane] : 0;
+            }
+            const int32_t pos = (int32_t)bounded(readlane64(wr1, h - hbase), (uint64_t)wsize);
+            const int32_t item = __builtin_amdgcn_readlane(win, pos);
+            const int64_t ti = __builtin_amdgcn_readlane(wint, pos);
+            int32_t up, upt;
+            if (w <= 16) {  // row_shl:1 -- lane i reads lane i + 1 of its 16-lane row
+                up = __builtin_amdgcn_update_dpp(win, win, 0x101, 0xF, 0xF, false);
+                upt = __builtin_amdgcn_update_dpp(wint, wint, 0x101, 0xF, 0xF, false);
+            } else {
+                up = __shfl_down(win, 1, kWave);
+                upt = __shfl_down(wint, 1, kWave);
+            }
+            if (lane >= pos && lane < wsize - 1) {
+                win = up;
+                wint = upt;
+            }
+            if (next < N) {
+                if (next - sbase == kWave) {
+                    sbase += kWave;
+                    sreg = sbase + lane < N ? a.sigma[sbase + lane] : 0;
+                    streg = sbase + lane < N ? a.t[sreg] : 0;
+                }
+                const int32_t ni = __builtin_amdgcn_readlane(sreg, next - sbase);
+                const int32_t nt = __builtin_amdgcn_readlane(streg, next - sbase);
+                if (lane == wsize - 1) {
+                    win = ni;
+                    wint = nt;
+                }
+                ++next;
+            } else {
+                if (lane == wsize - 1) {
+                    win = -1;
+                    wint = 0;
+                }
+                --wsize;
+            }
+            int32_t c;
+            if (h < K) {
+                c = h;
+            } else {
+                uint64_t best = 0;
+                int32_t nf = 0;
+                bool fe[NCH];
+#pragma unroll
+                for (int u = 0; u < NCH; ++u) {
+                    fe[u] = u * kWave + lane < K && Tr[u] + ti <= a.C;
+                    nf += __popcll(__ballot(fe[u]));
+                    if (fe[u] && kr[u] > best) best = kr[u];
+                }
+                if (nf == 0) {
+                    good = 0;
+                    break;
+                }
+                best = wave_max_u64(best);
+                const int32_t wp = w < nf ? w : nf;
+                const int32_t rho = (int32_t)bounded(readlane64(wr2, h - hbase), (uint64_t)wp);
+                for (int32_t pass = 1; pass <= rho; ++pass) {
+                    const uint64_t prev = best;
+                    best = 0;
+#pragma unroll
+                    for (int u = 0; u < NCH; ++u)
+                        if (fe[u] && kr[u] < prev && kr[u] > best) best = kr[u];
+                    best = wave_max_u64(best);
+                }
+                c = 0xFFFF - (int32_t)(best & 0xFFFF);
+            }
+#pragma unroll
+            for (int u = 0; u < NCH; ++u)
+                if (u * kWave + lane == c) {
+                    Tr[u] += ti;
+                    nr[u] += 1;
+                    kr[u] = fit_key(Tr[u], nr[u], c);
+                }
+            if (lane == 0) cellk[item] = c;
+        }
+#pragma unroll
+        for (int u = 0; u < NCH; ++u)
+            if (u * kWave + lane < K) cnt_s[u * kWave + lane] = nr[u];
+    }
+    if (lane == 0) a.ok[b] = good;
+    if (!good) return;
+    __syncthreads();
+    int32_t *ms = pf.mstart + (int64_t)b * (K + 1);
+    int32_t *ml = pf.mlist + (int64_t)b * N;
+    int64_t carry = 0;
+    for (int32_t cb = 0; cb < K; cb += kWave) {
+        const int32_t cc = cb + lane;
+        const int64_t v = cc < K ? cnt_s[cc] : 0;
+        const int64_t incl = wave_incl_scan(v);
+        if (cc < K) {
+            ms[cc] = (int32_t)(carry + incl - v);
+            cur[cc] = (int32_t)(carry + incl - v);
+        }
+        carry += (int64_t)readlane64((uint64_t)incl, kWave - 1);
+    }
+    if (lane == 0) ms[K] = N;
+    __syncthreads();
+    for (int32_t i = lane; i < N; i += kWave) {
+        const int32_t c = cellk[i];
+        ml[atomicAdd(&cur[c], 1)] = i;
+    }
+}
+
 // Q_k and peak_k of cell k = blockIdx.x of candidate b = blockIdx.y.
 __global__ void __launch_bounds__(128) k_pack_cellsum(TrialArgs a, PackFast pf) {
     extern __shared__ int32_t sq[];
@@ -609,7 +768,13 @@ __global__ void __launch_bounds__(256) k_pack_pair(TrialArgs a, PackFast pf) {
     for (int32_t e = tid; e < LP; e += nt) qb[e] = Qc[(int64_t)order[0] * LP + e];
     __syncthreads();
     constexpr int kPre = 16;  // Q entries per thread held for the next step (LP <= 16 * 256)
+    uint64_t wpair = 0;       // wave 0: pairing draws of steps pbase .. pbase + 63, one per lane
+    int32_t pbase = -kWave;
     for (int32_t pos = 0; pos < K; ++pos) {
+        if (wv == 0 && wd && pos - pbase == kWave) {
+            pbase = pos;
+            wpair = pos + lane < K ? wd[2 * (int64_t)N + pos + lane] : 0;
+        }
         const int32_t k = order[pos];
         const int32_t *qk = qb + (pos & 1) * LP;
         // next cell's Q row into registers while this step runs
@@ -674,7 +839,7 @@ __global__ void __launch_bounds__(256) k_pack_pair(TrialArgs a, PackFast pf) {
             int32_t rho = 0;
             if (wp > 1) {
                 const uint64_t total = (((uint64_t)1) << wp) - 1;
-                const uint64_t pick = bounded(wd[2 * (int64_t)N + pos], total);
+                const uint64_t pick = bounded(readlane64(wpair, pos - pbase), total);
                 uint64_t pref = 0;
                 for (rho = 0; rho < wp; ++rho) {
                     pref += ((uint64_t)1) << (wp - 1 - rho);
@@ -955,7 +1120,11 @@ extern "C" int routepack_pack_rows(const routepack_problem *prob, const int32_t 
         RP_HIP(hipFuncSetAttribute((const void *)k_pack_fit, hipFuncAttributeMaxDynamicSharedMemorySize, (int)fit_lds));
         RP_HIP(hipFuncSetAttribute((const void *)k_pack_pair, hipFuncAttributeMaxDynamicSharedMemorySize,
                                    (int)pair_lds));
-        hipLaunchKernelGGL(k_pack_fit, dim3(nb), dim3(64), fit_lds, stream, ta, pf);
+        if (K <= 8 * kWave) {
+            hipLaunchKernelGGL(k_pack_fit_reg<8>, dim3(nb), dim3(64), (size_t)8 * K, stream, ta, pf);
+        } else {
+            hipLaunchKernelGGL(k_pack_fit, dim3(nb), dim3(64), fit_lds, stream, ta, pf);
+        }
         hipLaunchKernelGGL(k_pack_cellsum, dim3(K, nb), dim3(128), (size_t)4 * LP, stream, ta, pf);
         hipLaunchKernelGGL(k_pack_pair, dim3(nb), dim3(256), (size_t)pair_lds, stream, ta, pf);
     } else {
