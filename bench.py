@@ -50,11 +50,25 @@ def pmc_file(kernel, window):
     return os.path.join(ROOT, "profiles", f"anneal_{kernel}_{window}_pmc.txt")
 
 
+def _code_text(src: str) -> str:
+    """The source with // comments and blank lines removed (comment edits do
+    not change the kernel the counters were taken on)."""
+    out = []
+    for line in src.splitlines():
+        i = line.find("//")
+        if i >= 0 and line.count('"', 0, i) % 2 == 0:
+            line = line[:i]
+        line = line.rstrip()
+        if line:
+            out.append(line)
+    return "\n".join(out)
+
+
 def kernel_source_hash(kernel) -> str:
     h = hashlib.sha256()
     for f in kernel_sources(kernel):
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+        with open(f, encoding="utf-8") as fh:
+            h.update(_code_text(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

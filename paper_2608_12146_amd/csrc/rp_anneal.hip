@@ -1084,11 +1084,14 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
     (void)xscore_in;
 
     // Kernel choice: one wave per member when its state fits LDS (members
-    // updated in place, slabs handed over at resampling) -- the chain kernel
-    // when the shape fits its lane layout, else the flat wave kernel --, else
-    // one workgroup per member over double-buffered slabs.
-    // ROUTEPACK_ANNEAL_KERNEL=chain|wave|workgroup requests one kernel; a
-    // request the problem does not fit fails with ROUTEPACK_E_UNSUPPORTED.
+    // updated in place, slabs handed over at resampling) -- the chain kernels
+    // when the shape fits their lane layout (the whole schedule in one
+    // cooperative launch when every workgroup can stay resident, else one
+    // launch per level), else the flat wave kernel --, else one workgroup per
+    // member over double-buffered slabs.
+    // ROUTEPACK_ANNEAL_KERNEL=chain_run|chain|wave|workgroup requests one
+    // kernel; a request the problem does not fit fails with
+    // ROUTEPACK_E_UNSUPPORTED.
     int32_t mpw = 0, chain_pv = 0, chain_dv = 0;
     bool tlds = false;
     const char *force = getenv("ROUTEPACK_ANNEAL_KERNEL");
