@@ -87,7 +87,42 @@ struct Screen {
 
 __device__ inline int32_t clamp0(int32_t v, int32_t hi) { return v < 0 ? 0 : (v > hi ? hi : v); }
 
+// floor(w m / 2^64) for m < 2^32 (lane-varying m): hi(w) m plus the carry
+// word floor(lo(w) m / 2^32), shifted down; both products are 32 x 32.
+__device__ inline uint32_t bounded_small(uint64_t w, uint32_t m) {
+    const uint64_t lo = (uint64_t)__umulhi((uint32_t)w, m);
+    return (uint32_t)(((uint64_t)(uint32_t)(w >> 32) * m + lo) >> 32);
+}
+
+// A wave-uniform 64-bit value as scalar registers.
+__device__ inline uint64_t uniform64(uint64_t v) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(v >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// floor(w m / 2^64) for a wave-uniform m (the branch on its size is scalar).
+__device__ inline uint64_t bounded_uniform(uint64_t w, uint64_t m) {
+    m = uniform64(m);
+    if ((m >> 32) == 0) return bounded_small(w, (uint32_t)m);
+    return __umul64hi(w, m);
+}
+
+// Ends a stage of independent LDS reads: every value listed is waited for
+// here, so the reads of a stage go out together (one round trip) instead of
+// being interleaved with the arithmetic that consumes them.
+template <typename T>
+__device__ inline void stage_one(T &v) {
+    asm volatile("" : "+v"(v));
+}
+template <typename... T>
+__device__ inline void stage_end(T &...v) {
+    (stage_one(v), ...);
+}
+
 // Resolves the proposal of this lane against the member's current state.
+// The reads go out in dependent stages; the uniform-mode proposal's reads
+// ride along with the first two stages of the guided chain.
 template <int DV>
 __device__ inline Screen screen(const AnnealArgs &a, const Lds &M, const Tables &tb, uint64_t w0, uint64_t w1,
                                 uint64_t w2, uint64_t w3, uint64_t w4, uint64_t w5, uint64_t w6, int64_t s1,
@@ -96,84 +131,127 @@ __device__ inline Screen screen(const AnnealArgs &a, const Lds &M, const Tables 
     const int32_t N = a.N, B = a.B, RG = a.RG, D = a.D, G = a.G;
     const bool guided = (uint32_t)w0 < a.p_guide;
     const bool reloc = (uint32_t)(w0 >> 32) < a.rho;
-    // Uniform-mode proposal: samples (and the target cell of a relocation)
-    // straight from the words; its reads go out first.
-    const int32_t ir = (int32_t)bounded(w1, (uint64_t)N);
-    const int32_t jr = (int32_t)bounded(w4, (uint64_t)N);
-    const int32_t cir = clamp0(M.cell[ir], B - 1), cjr = clamp0(M.cell[jr], B - 1);
-    const int32_t tir = tb.t[ir], tjr = tb.t[jr];
-    int32_t c1 = cir, c2 = reloc ? (int32_t)bounded(w4, (uint64_t)B) : cjr;
-    int32_t T1 = M.T[c1], T2 = M.T[c2];
-    int32_t sz1 = (int32_t)M.start[c1 + 1] - (int32_t)M.start[c1];
-    int32_t i = ir, j = reloc ? -1 : jr;
-    int32_t ti = tir, tj = reloc ? 0 : tjr;
-    sc.pos_i = -1;
-    sc.pos_j = -1;
-    if (__ballot(guided)) {
-        // Source row-shard: roulette over J; target: over s2 - J_h + 1, whose
-        // prefix is V_h = (h + 1)(s2 + 1) - J_pre[h].  Both prefixes are
-        // non-decreasing: count the pivots, then the entries of one block.
-        const uint64_t pk1 = bounded(w1, (uint64_t)s1);
-        const uint64_t pk4 = bounded(w4, (uint64_t)((int64_t)RG * (s2 + 1) - s1));
-        int32_t k1 = 0, k4 = 0;
+    // Uniform-mode samples (and target cell of a relocation) straight from
+    // the words (N, B < 2^16).
+    const int32_t ir = (int32_t)bounded_small(w1, (uint32_t)N);
+    const int32_t jr = (int32_t)bounded_small(w4, (uint32_t)N);
+    const int32_t rc2 = (int32_t)bounded_small(w4, (uint32_t)B);
+    // Guided: source row-shard by roulette over J, target over s2 - J_h + 1,
+    // whose prefix is V_h = (h + 1)(s2 + 1) - J_pre[h].  Both prefixes are
+    // non-decreasing: count the pivots J_pre[8k + 7], then the entries of one
+    // block.
+    const uint64_t pk1 = bounded_uniform(w1, (uint64_t)s1);
+    const uint64_t pk4 = bounded_uniform(w4, (uint64_t)((int64_t)RG * (s2 + 1) - s1));
+    // stage 1: pivots; the uniform-mode cells and lengths
+    int64_t jp[8], vp[8];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            k1 += (uint64_t)M.Jpiv[k] <= pk1 ? 1 : 0;
-            k4 += (uint64_t)M.Vpiv[k] <= pk4 ? 1 : 0;
-        }
-        int32_t h1 = 8 * k1, h4 = 8 * k4;
-        const int64_t *f1 = M.Jpre + 8 * k1, *f4 = M.Vpre + 8 * k4;
+    for (int k = 0; k < 8; ++k) {
+        jp[k] = M.Jpiv[k];
+        vp[k] = M.Vpiv[k];
+    }
+    int32_t cir = M.cell[ir], cjr = M.cell[jr];
+    int32_t tir = tb.t[ir], tjr = tb.t[jr];
+    stage_end(jp[0], jp[1], jp[2], jp[3], jp[4], jp[5], jp[6], jp[7], vp[0], vp[1], vp[2], vp[3], vp[4], vp[5],
+              vp[6], vp[7], cir, cjr, tir, tjr);
+    int32_t k1 = 0, k4 = 0;
 #pragma unroll
-        for (int x = 0; x < 8; ++x) {
-            h1 += (uint64_t)f1[x] <= pk1 ? 1 : 0;
-            h4 += (uint64_t)f4[x] <= pk4 ? 1 : 0;
-        }
-        if (s1 == 0) h1 = (int32_t)bounded(w1, (uint64_t)RG);
-        h1 = clamp0(h1, RG - 1);
-        h4 = clamp0(h4, RG - 1);
-        // Source cell: roulette over the row-shard's cell costs (prefix padded
-        // with kInf past its slots); target cell: uniform over its slots.
-        const int64_t *cp = M.Cp + h1 * DV;
-        int64_t cv[DV];
+    for (int k = 0; k < 8; ++k) {
+        k1 += (uint64_t)jp[k] <= pk1 ? 1 : 0;
+        k4 += (uint64_t)vp[k] <= pk4 ? 1 : 0;
+    }
+    k1 = k1 < 7 ? k1 : 7;  // (8 only when s1 == 0, whose pick is redrawn below)
+    k4 = k4 < 7 ? k4 : 7;
+    const int32_t uc1 = clamp0(cir, B - 1);
+    const int32_t uc2 = reloc ? rc2 : clamp0(cjr, B - 1);
+    // stage 2: the two blocks; the uniform-mode cell loads and sizes
+    int64_t jb[8], vb[8];
 #pragma unroll
-        for (int x = 0; x < DV; ++x) cv[x] = cp[x];
-        const int64_t tot = M.Ctot[h1];
-        const int32_t cnt1 = tb.hcnt[h1], cnt2 = tb.hcnt[h4];
-        int32_t xi;
-        if (tot == 0) {
-            xi = (int32_t)bounded(w2, (uint64_t)cnt1);
-        } else {
-            const uint64_t pk2 = bounded_lane(w2, (uint64_t)tot);
-            xi = 0;
+    for (int x = 0; x < 8; ++x) {
+        jb[x] = M.Jpre[8 * k1 + x];
+        vb[x] = M.Vpre[8 * k4 + x];
+    }
+    int32_t uT1 = M.T[uc1], uT2 = M.T[uc2];
+    int32_t us0 = M.start[uc1], us1 = M.start[uc1 + 1];
+    stage_end(jb[0], jb[1], jb[2], jb[3], jb[4], jb[5], jb[6], jb[7], vb[0], vb[1], vb[2], vb[3], vb[4], vb[5],
+              vb[6], vb[7], uT1, uT2, us0, us1);
+    int32_t h1 = 8 * k1, h4 = 8 * k4;
 #pragma unroll
-            for (int x = 0; x < DV; ++x) xi += (uint64_t)cv[x] <= pk2 ? 1 : 0;
-        }
-        xi = clamp0(xi, cnt1 - 1);
-        const int32_t x2 = (int32_t)bounded(w5, (uint64_t)cnt2);
-        const int32_t gc1 = clamp0(G == 1 ? h1 * D + xi : tb.hcell[h1 * DV + xi], B - 1);
-        const int32_t gc2 = clamp0(G == 1 ? h4 * D + x2 : tb.hcell[h4 * DV + x2], B - 1);
-        const int32_t st1 = M.start[gc1], en1 = M.start[gc1 + 1];
-        const int32_t st2 = M.start[gc2], en2 = M.start[gc2 + 1];
-        const int32_t gT1 = M.T[gc1], gT2 = M.T[gc2];
-        const int32_t pi = clamp0(st1 + (int32_t)bounded(w3, (uint64_t)(en1 - st1)), N - 1);
-        const int32_t pj = clamp0(st2 + (int32_t)bounded(w6, (uint64_t)(en2 - st2)), N - 1);
-        const int32_t gi = M.pool[pi], gj = M.pool[pj];
-        const int32_t gti = tb.t[gi], gtj = tb.t[gj];
-        if (guided) {
-            c1 = gc1;
-            c2 = gc2;
-            T1 = gT1;
-            T2 = gT2;
-            sz1 = en1 - st1;
-            i = gi;
-            ti = gti;
-            sc.pos_i = pi;
-            if (!reloc) {
-                j = gj;
-                tj = gtj;
-                sc.pos_j = pj;
-            }
-        }
+    for (int x = 0; x < 8; ++x) {
+        h1 += (uint64_t)jb[x] <= pk1 ? 1 : 0;
+        h4 += (uint64_t)vb[x] <= pk4 ? 1 : 0;
+    }
+    if (s1 == 0) h1 = (int32_t)bounded_small(w1, (uint32_t)RG);
+    h1 = clamp0(h1, RG - 1);
+    h4 = clamp0(h4, RG - 1);
+    // stage 3: source cell roulette over the row-shard's cell costs (prefix
+    // padded with kInf past its slots); target cell uniform over its slots
+    int64_t cv[DV];
+#pragma unroll
+    for (int x = 0; x < DV; ++x) cv[x] = M.Cp[h1 * DV + x];
+    int64_t tot = M.Ctot[h1];
+    int32_t cnt1 = tb.hcnt[h1], cnt2 = tb.hcnt[h4];
+    stage_end(tot, cnt1, cnt2);
+#pragma unroll
+    for (int x = 0; x < DV; ++x) stage_end(cv[x]);
+    int32_t xi;
+    if (tot == 0) {
+        xi = (int32_t)bounded_small(w2, (uint32_t)cnt1);
+    } else {
+        const uint64_t pk2 = __umul64hi(w2, (uint64_t)tot);
+        xi = 0;
+#pragma unroll
+        for (int x = 0; x < DV; ++x) xi += (uint64_t)cv[x] <= pk2 ? 1 : 0;
+    }
+    xi = clamp0(xi, cnt1 - 1);
+    const int32_t x2 = (int32_t)bounded_small(w5, (uint32_t)cnt2);
+    int32_t gc1, gc2;
+    if (G == 1) {
+        gc1 = clamp0(h1 * D + xi, B - 1);
+        gc2 = clamp0(h4 * D + x2, B - 1);
+    } else {
+        gc1 = tb.hcell[h1 * DV + xi];
+        gc2 = tb.hcell[h4 * DV + x2];
+        stage_end(gc1, gc2);
+        gc1 = clamp0(gc1, B - 1);
+        gc2 = clamp0(gc2, B - 1);
+    }
+    // stage 4: member ranges and loads of both cells
+    int32_t st1 = M.start[gc1], en1 = M.start[gc1 + 1];
+    int32_t st2 = M.start[gc2], en2 = M.start[gc2 + 1];
+    int32_t gT1 = M.T[gc1], gT2 = M.T[gc2];
+    stage_end(st1, en1, st2, en2, gT1, gT2);
+    const int32_t pi = clamp0(st1 + (int32_t)bounded_small(w3, (uint32_t)(en1 - st1)), N - 1);
+    const int32_t pj = clamp0(st2 + (int32_t)bounded_small(w6, (uint32_t)(en2 - st2)), N - 1);
+    // stage 5: the samples; stage 6: their lengths
+    int32_t gi = M.pool[pi], gj = M.pool[pj];
+    stage_end(gi, gj);
+    int32_t gti = tb.t[gi], gtj = tb.t[gj];
+    stage_end(gti, gtj);
+    int32_t c1, c2, T1, T2, sz1, i, j, ti, tj;
+    if (guided) {
+        c1 = gc1;
+        c2 = gc2;
+        T1 = gT1;
+        T2 = gT2;
+        sz1 = en1 - st1;
+        i = gi;
+        ti = gti;
+        sc.pos_i = pi;
+        j = reloc ? -1 : gj;
+        tj = reloc ? 0 : gtj;
+        sc.pos_j = reloc ? -1 : pj;
+    } else {
+        c1 = uc1;
+        c2 = uc2;
+        T1 = uT1;
+        T2 = uT2;
+        sz1 = us1 - us0;
+        i = ir;
+        ti = tir;
+        sc.pos_i = -1;
+        j = reloc ? -1 : jr;
+        tj = reloc ? 0 : tjr;
+        sc.pos_j = -1;
     }
     bool f = c1 != c2;
     if (f) {
@@ -535,6 +613,29 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
     const int half = lane >> 5, hl = lane & 31, cx = lane & 15;
     const bool lay_act = hl < L;  // lane holds layer hl of row-shard a / b
     const bool cell_lane = (lane & 16) == 0;
+    // Rows of the W and q loads of one move: lane (half, hl) reads layer hl
+    // of row-shard ha (half 0) or hb (half 1) and of the q rows of i and j
+    // (j < 0: zeros).
+    auto load_rows = [&](int32_t i, int32_t j, int32_t ha, int32_t hb, int4 *wr, int4 *qa, int4 *qb) {
+        const int32_t row = half ? hb : ha, ll = lay_act ? hl : L - 1;
+        const int4 *wp = reinterpret_cast<const int4 *>(W + ((int64_t)row * L + ll) * PV);
+        const int4 *qip = reinterpret_cast<const int4 *>(a.q + ((int64_t)i * L + ll) * PV);
+#pragma unroll
+        for (int x = 0; x < PV / 4; ++x) {
+            wr[x] = wp[x];
+            qa[x] = qip[x];
+        }
+        // (zeros on a path of their own: overwriting loaded registers would
+        // wait for the loads)
+        if (j >= 0) {
+            const int4 *qjp = reinterpret_cast<const int4 *>(a.q + ((int64_t)j * L + ll) * PV);
+#pragma unroll
+            for (int x = 0; x < PV / 4; ++x) qb[x] = qjp[x];
+        } else {
+#pragma unroll
+            for (int x = 0; x < PV / 4; ++x) qb[x] = make_int4(0, 0, 0, 0);
+        }
+    };
 
     for (int32_t k0 = 0; k0 < a.K; k0 += kWave) {
         const int32_t k = k0 + lane;
@@ -574,22 +675,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
             const bool two = ha != hb;
             // W rows of a and b, q rows of i and j: issue the loads first.
             int4 wr[PV / 4], qa[PV / 4], qb[PV / 4];
-            if (two) {
-                const int32_t row = half ? hb : ha, ll = lay_act ? hl : L - 1;
-                const int4 *wp = reinterpret_cast<const int4 *>(W + ((int64_t)row * L + ll) * PV);
-                const int4 *qip = reinterpret_cast<const int4 *>(a.q + ((int64_t)i * L + ll) * PV);
-                const int4 *qjp = reinterpret_cast<const int4 *>(a.q + ((int64_t)(j >= 0 ? j : i) * L + ll) * PV);
-#pragma unroll
-                for (int x = 0; x < PV / 4; ++x) {
-                    wr[x] = wp[x];
-                    qa[x] = qip[x];
-                    qb[x] = qjp[x];
-                }
-                if (j < 0) {
-#pragma unroll
-                    for (int x = 0; x < PV / 4; ++x) qb[x] = make_int4(0, 0, 0, 0);
-                }
-            }
+            if (two) load_rows(i, j, ha, hb, wr, qa, qb);
             // Commit inputs, read now so they overlap the row loads: the member
             // ranges of both cells and, when both fit 32 lanes, their members
             // (half 0: c1, half 1: c2).
@@ -1000,7 +1086,7 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
     }
     unsigned epoch = 0;
     const uint64_t P = (uint64_t)pop;
-    const int64_t nW16 = (int64_t)a.RG * a.LP / 4;  // W of a slab in 16-byte units
+    const int32_t nW16 = a.RG * a.LP / 4;  // W of a slab in 16-byte units
     for (int n = 0; n < r.n_sweeps; ++n) {
         const int32_t level = r.offset + n;
         const double temp = r.temps[n];
@@ -1167,28 +1253,31 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
             // Every further child gets its parent's W in its own slab; the
             // copies are split evenly over all workgroups.
             {
+                // units <= pop * nW16 < 2^31: nW16 <= 64 * 32 * 16 / 4 and the
+                // level-end tables in LDS hold pop below 6000
                 const int32_t *dups = reinterpret_cast<const int32_t *>(Fs);
-                const int64_t units = (int64_t)tdup * nW16;
-                const int64_t share = (units + nb - 1) / nb;
-                const int64_t u0 = (int64_t)blockIdx.x * share, u1 = u0 + share < units ? u0 + share : units;
+                const int32_t units = (int32_t)tdup * nW16;
+                const int32_t share = (units + nb - 1) / nb;
+                const int32_t u0 = blockIdx.x * share, u1 = u0 + share < units ? u0 + share : units;
                 constexpr int U = 4;
-                for (int64_t base = u0; base < u1; base += U * nt) {
-                    int4 v[U];
-                    int4 *dst[U];
+                for (int32_t base = u0; base < u1; base += U * nt) {
+                    // every slot loads (clamped to the last unit), so all U
+                    // loads are in flight before the first store
+                    typedef int32_t v4i __attribute__((ext_vector_type(4)));
+                    v4i v[U];
+                    int64_t dsto[U];
 #pragma unroll
                     for (int u = 0; u < U; ++u) {
-                        const int64_t x = base + u * nt + tid;
-                        dst[u] = nullptr;
-                        if (x < u1) {
-                            const int32_t c = dups[x / nW16];
-                            const int64_t off = x - (x / nW16) * nW16;
-                            v[u] = reinterpret_cast<const int4 *>(a.slabs + (int64_t)slab[par[c]] * a.off.bytes + a.off.W)[off];
-                            dst[u] = reinterpret_cast<int4 *>(a.slabs + (int64_t)slabn[c] * a.off.bytes + a.off.W) + off;
-                        }
+                        const int32_t x = base + u * nt + tid < u1 ? base + u * nt + tid : u1 - 1;
+                        const int32_t ci = (int32_t)((uint32_t)x / (uint32_t)nW16);
+                        const int32_t off = x - ci * nW16;
+                        const int32_t c = dups[ci];
+                        v[u] = reinterpret_cast<const v4i *>(a.slabs + (int64_t)slab[par[c]] * a.off.bytes + a.off.W)[off];
+                        dsto[u] = (int64_t)slabn[c] * a.off.bytes + a.off.W + (int64_t)off * 16;
                     }
 #pragma unroll
                     for (int u = 0; u < U; ++u)
-                        if (dst[u]) *dst[u] = v[u];
+                        if (base + u * nt + tid < u1) *reinterpret_cast<v4i *>(a.slabs + dsto[u]) = v[u];
                 }
             }
             // and the rest of its state from the parent's own slab
