@@ -52,6 +52,8 @@ struct AnnealArgs {
     int32_t scale_pow2;         // 2^F C is a power of two
     double inv_scale;           // 1 / (2^F C) when it is
     unsigned long long *phase_cycles;  // [pop][8] with RP_PHASE_TIMERS builds, else unused
+    const int32_t *qzero;       // [L * P] zeros (chain kernels: the q row of "no sample")
+    int32_t sum32;              // L * (W entry bound) < 2^31: per-row layer sums fit int32
 };
 
 // Wave kernel plan and launchers (rp_anneal_wave.hip).
@@ -74,7 +76,13 @@ struct RunArgs {
     int64_t *wg_best;      // [workgroups][4] lexicographic-min trajectory best and its member
     double *wg_emin;       // [workgroups] minimum terminal energy
     int32_t o_lend;        // LDS offset of the level-end tables
+    char *blobs;           // [pop][blob_bytes]: a published member's LDS image and registers, per slab
+    int64_t blob_bytes;
 };
+
+// Bytes of one hand-over image: the member's LDS region, then J, A and U of
+// every lane and the score.
+inline int64_t run_blob_bytes(int32_t lds_member) { return ((int64_t)lds_member + 8 * (3 * 64 + 3) + 255) & ~(int64_t)255; }
 
 // Chain kernel plan and launchers (rp_anneal_chain.hip).
 bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out, int32_t *dv_out);

@@ -983,7 +983,9 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
     int64_t *chk_score = scr.get<int64_t>(3);
     int32_t *chk = scr.get<int32_t>(2);
     int64_t *xscore_in = scr.get<int64_t>(3);
+    int32_t *qzero = scr.get<int32_t>(LP64 > 0 ? LP64 : 1);
     if (scr.failed()) return ROUTEPACK_E_DEVICE;
+    RP_HIP(hipMemsetAsync(qzero, 0, sizeof(int32_t) * (LP64 > 0 ? LP64 : 1), stream));
 
     AnnealArgs a;
     memset(&a, 0, sizeof(a));
@@ -1006,6 +1008,8 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
         a.beta[s] = prob->beta_fp[s];
     }
     a.slots = dp.slots; a.count = dp.count; a.slot_shard = dp.slot_shard;
+    a.qzero = qzero;
+    a.sum32 = (long double)L * (long double)w_entry_bound(prob, ws) < 2147483648.0L ? 1 : 0;
     a.off = off;
     a.best = best; a.results = results;
     a.seed = prm->seed; a.p_guide = prm->p_guide_u32; a.rho = prm->rho_u32;
@@ -1168,6 +1172,8 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
         double *energy_d = scr.get<double>(pop_size);
         int64_t *wg_best = scr.get<int64_t>((size_t)4 * pop_size);
         double *wg_emin = scr.get<double>(pop_size);
+        const int64_t blob_bytes = run_blob_bytes(a.lds_member);
+        char *blobs = scr.get<char>((size_t)pop_size * (size_t)blob_bytes);
         if (scr.failed()) return ROUTEPACK_E_DEVICE;
         RP_HIP(hipMemcpyAsync(temps_d, prm->temperatures, sizeof(double) * prm->n_sweeps, hipMemcpyHostToDevice,
                               stream));
@@ -1189,6 +1195,8 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
         run.energy = energy_d;
         run.wg_best = wg_best;
         run.wg_emin = wg_emin;
+        run.blobs = blobs;
+        run.blob_bytes = blob_bytes;
         hipEvent_t e0 = nullptr, e1 = nullptr;
         if (prm->level_kernel_ms) {
             RP_HIP(hipEventCreate(&e0));

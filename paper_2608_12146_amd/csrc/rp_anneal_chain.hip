@@ -613,27 +613,21 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
     const int half = lane >> 5, hl = lane & 31, cx = lane & 15;
     const bool lay_act = hl < L;  // lane holds layer hl of row-shard a / b
     const bool cell_lane = (lane & 16) == 0;
-    // Rows of the W and q loads of one move: lane (half, hl) reads layer hl
-    // of row-shard ha (half 0) or hb (half 1) and of the q rows of i and j
-    // (j < 0: zeros).
-    auto load_rows = [&](int32_t i, int32_t j, int32_t ha, int32_t hb, int4 *wr, int4 *qa, int4 *qb) {
+    // Loads of one move: lane (half, hl) reads layer hl of row-shard ha
+    // (half 0) or hb (half 1), the q row that leaves that row-shard (qx) and
+    // the one that enters it (qy), so every lane's new row is wr - qx + qy.
+    // A relocation moves no sample back: its missing row is the zero row.
+    auto load_rows = [&](int32_t i, int32_t j, int32_t ha, int32_t hb, int4 *wr, int4 *qx, int4 *qy) {
         const int32_t row = half ? hb : ha, ll = lay_act ? hl : L - 1;
+        const int32_t *qi = a.q + (int64_t)i * a.LP, *qj = j >= 0 ? a.q + (int64_t)j * a.LP : a.qzero;
         const int4 *wp = reinterpret_cast<const int4 *>(W + ((int64_t)row * L + ll) * PV);
-        const int4 *qip = reinterpret_cast<const int4 *>(a.q + ((int64_t)i * L + ll) * PV);
+        const int4 *xp = reinterpret_cast<const int4 *>((half ? qj : qi) + ll * PV);
+        const int4 *yp = reinterpret_cast<const int4 *>((half ? qi : qj) + ll * PV);
 #pragma unroll
         for (int x = 0; x < PV / 4; ++x) {
             wr[x] = wp[x];
-            qa[x] = qip[x];
-        }
-        // (zeros on a path of their own: overwriting loaded registers would
-        // wait for the loads)
-        if (j >= 0) {
-            const int4 *qjp = reinterpret_cast<const int4 *>(a.q + ((int64_t)j * L + ll) * PV);
-#pragma unroll
-            for (int x = 0; x < PV / 4; ++x) qb[x] = qjp[x];
-        } else {
-#pragma unroll
-            for (int x = 0; x < PV / 4; ++x) qb[x] = make_int4(0, 0, 0, 0);
+            qx[x] = xp[x];
+            qy[x] = yp[x];
         }
     };
 
@@ -674,13 +668,30 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
             const int32_t ha = ra * G + ga, hb = rb * G + gb;
             const bool two = ha != hb;
             // W rows of a and b, q rows of i and j: issue the loads first.
-            int4 wr[PV / 4], qa[PV / 4], qb[PV / 4];
-            if (two) load_rows(i, j, ha, hb, wr, qa, qb);
-            // Commit inputs, read now so they overlap the row loads: the member
-            // ranges of both cells and, when both fit 32 lanes, their members
-            // (half 0: c1, half 1: c2).
-            const int32_t st1 = M.start[c1], en1 = M.start[c1 + 1];
-            const int32_t st2 = M.start[c2], en2 = M.start[c2 + 1];
+            int4 wr[PV / 4], qx[PV / 4], qy[PV / 4];
+            if (two) load_rows(i, j, ha, hb, wr, qx, qy);
+            // Cell statistics of the two row-shards (lanes (half, cx)) and the
+            // commit inputs, read in one stage while the row loads are in
+            // flight: the member ranges of both cells and, when both fit 32
+            // lanes, their members (half 0: c1, half 1: c2; left in flight
+            // until the commit).
+            const int32_t hsel = half ? hb : ha;
+            int32_t cnt = D, cc = hsel * D + cx;  // (one EDP shard: every row-shard is a row of D slots)
+            if (G != 1) {
+                cnt = tb.hcnt[hsel];
+                cc = tb.hcell[hsel * DV + (cx < DV ? cx : 0)];
+                stage_end(cnt, cc);
+            }
+            const bool cact = cell_lane && cx < cnt && (half == 0 || two);
+            int32_t st1 = M.start[c1], en1 = M.start[c1 + 1];
+            int32_t st2 = M.start[c2], en2 = M.start[c2 + 1];
+            int64_t Tc = 0, Qc = 0;
+            if (cact) {
+                Tc = M.T[cc];
+                Qc = M.Q[cc];
+            }
+            int64_t T1 = M.T[c1], T2 = M.T[c2], Q1 = M.Q[c1], Q2v = M.Q[c2];
+            stage_end(st1, en1, st2, en2, Tc, Qc, T1, T2, Q1, Q2v);
             const int32_t sz1 = en1 - st1, sz2 = en2 - st2;
             const bool small = sz1 <= 32 && sz2 <= 32;
             int32_t y = -1;
@@ -690,16 +701,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                 yv = hl < sz;
                 if (yv) y = M.pool[(half ? st2 : st1) + hl];
             }
-            // cell statistics of the two row-shards (lanes (half, cx))
-            const int32_t hsel = half ? hb : ha;
-            const int32_t cnt = tb.hcnt[hsel];
-            const bool cact = cell_lane && cx < cnt && (half == 0 || two);
-            int64_t Tc = 0, Qc = 0;
-            int32_t cc = -1;
             if (cact) {
-                cc = G == 1 ? hsel * D + cx : tb.hcell[hsel * DV + cx];
-                Tc = M.T[cc];
-                Qc = M.Q[cc];
                 if (cc == c1) {
                     Tc += tj - ti;
                     Qc += tj * tj - ti * ti;
@@ -709,14 +711,16 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                     Qc += ti * ti - tj * tj;
                 }
             }
-            const int64_t T1 = M.T[c1], T2 = M.T[c2], Q1 = M.Q[c1], Q2v = M.Q[c2];
             const int64_t nT1 = T1 - ti + tj, nT2 = T2 + ti - tj;
             const int64_t nQ1 = Q1 - ti * ti + tj * tj, nQ2 = Q2v + ti * ti - tj * tj;
             int64_t Arow = 0, cw = 0;
-            for (int s = 0; s < a.S; ++s) {
-                const int64_t cost = a.alpha[s] * Tc + a.beta[s] * Qc;
-                cw += cact ? cost : 0;
-                Arow = (int64_t)((uint64_t)Arow + (uint64_t)row_max64(cact ? cost : LLONG_MIN));
+#pragma unroll
+            for (int s = 0; s < kMaxStages; ++s) {
+                if (s < a.S) {
+                    const int64_t cost = a.alpha[s] * Tc + a.beta[s] * Qc;
+                    cw += cact ? cost : 0;
+                    Arow = (int64_t)((uint64_t)Arow + (uint64_t)row_max64(cact ? cost : LLONG_MIN));
+                }
             }
             const int64_t Aa = (int64_t)readlane64((uint64_t)Arow, 0);
             const int64_t Ab = two ? (int64_t)readlane64((uint64_t)Arow, 32) : Aa;
@@ -728,25 +732,28 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                 int32_t mx = INT32_MIN;
 #pragma unroll
                 for (int x = 0; x < PV / 4; ++x) {
-                    const int32_t d0 = qa[x].x - qb[x].x, d1 = qa[x].y - qb[x].y;
-                    const int32_t d2 = qa[x].z - qb[x].z, d3 = qa[x].w - qb[x].w;
-                    nw[4 * x + 0] = half ? wr[x].x + d0 : wr[x].x - d0;
-                    nw[4 * x + 1] = half ? wr[x].y + d1 : wr[x].y - d1;
-                    nw[4 * x + 2] = half ? wr[x].z + d2 : wr[x].z - d2;
-                    nw[4 * x + 3] = half ? wr[x].w + d3 : wr[x].w - d3;
+                    nw[4 * x + 0] = wr[x].x - qx[x].x + qy[x].x;
+                    nw[4 * x + 1] = wr[x].y - qx[x].y + qy[x].y;
+                    nw[4 * x + 2] = wr[x].z - qx[x].z + qy[x].z;
+                    nw[4 * x + 3] = wr[x].w - qx[x].w + qy[x].w;
                 }
 #pragma unroll
                 for (int p = 0; p < PV; ++p) mx = nw[p] > mx ? nw[p] : mx;
-                const int64_t sm = row_sum64(lay_act ? (int64_t)mx : 0);
-                const int64_t suma = (int64_t)(readlane64((uint64_t)sm, 0) + readlane64((uint64_t)sm, 16));
-                const int64_t sumb = (int64_t)(readlane64((uint64_t)sm, 32) + readlane64((uint64_t)sm, 48));
+                int64_t suma, sumb;
+                if (a.sum32) {  // L times the W bound fits 31 bits
+                    const int32_t sm = row_sum32(lay_act ? mx : 0);
+                    suma = (int64_t)__builtin_amdgcn_readlane(sm, 0) + __builtin_amdgcn_readlane(sm, 16);
+                    sumb = (int64_t)__builtin_amdgcn_readlane(sm, 32) + __builtin_amdgcn_readlane(sm, 48);
+                } else {
+                    const int64_t sm = row_sum64(lay_act ? (int64_t)mx : 0);
+                    suma = (int64_t)(readlane64((uint64_t)sm, 0) + readlane64((uint64_t)sm, 16));
+                    sumb = (int64_t)(readlane64((uint64_t)sm, 32) + readlane64((uint64_t)sm, 48));
+                }
                 Ja = Aa + (suma << a.F);
                 Jb = Ab + (sumb << a.F);
             } else {
-                Ja = Aa + (Jha - Aha);
+                Ja = Aa + (Jha - Aha);  // (nw unused: W does not change)
                 Jb = Ja;
-#pragma unroll
-                for (int p = 0; p < PV; ++p) nw[p] = 0;
             }
             const int64_t dJa = Ja - Jha, dJb = two ? Jb - Jhb : 0;
             const int64_t n1 = s1 + dJa + dJb;
@@ -944,6 +951,69 @@ __global__ void __launch_bounds__(512) k_anneal_chain(AnnealArgs a) {
 namespace {
 
 constexpr unsigned kSpinLimit = 1u << 22;
+
+// Hand-over of a member to another wave through global memory: the raw LDS
+// region (16-byte units, all reads then all writes per batch) and the
+// registers.  Every lane of the wave takes part.
+typedef int32_t v4i __attribute__((ext_vector_type(4)));
+__device__ inline void member_publish(const AnnealArgs &a, const char *mine, char *blob, const Regs &R) {
+    const int lane = lane_id();
+    wsync();
+    const int32_t n16 = a.lds_member >> 4;
+    const v4i *src = reinterpret_cast<const v4i *>(mine);
+    v4i *dst = reinterpret_cast<v4i *>(blob);
+    constexpr int U = 8;
+    for (int32_t base = 0; base < n16; base += U * kWave) {
+        v4i v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int32_t x = base + u * kWave + lane;
+            v[u] = src[x < n16 ? x : n16 - 1];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int32_t x = base + u * kWave + lane;
+            if (x < n16) dst[x] = v[u];
+        }
+    }
+    int64_t *rg = reinterpret_cast<int64_t *>(blob + a.lds_member);
+    rg[lane] = R.Jr;
+    rg[kWave + lane] = R.Ar;
+    rg[2 * kWave + lane] = R.Ur;
+    if (lane == 0) {
+        rg[3 * kWave] = R.s0;
+        rg[3 * kWave + 1] = R.s1;
+        rg[3 * kWave + 2] = R.s2;
+    }
+}
+__device__ inline void member_receive(const AnnealArgs &a, char *mine, const char *blob, Regs &R) {
+    const int lane = lane_id();
+    const int32_t n16 = a.lds_member >> 4;
+    const v4i *src = reinterpret_cast<const v4i *>(blob);
+    v4i *dst = reinterpret_cast<v4i *>(mine);
+    const int64_t *rg = reinterpret_cast<const int64_t *>(blob + a.lds_member);
+    R.Jr = rg[lane];
+    R.Ar = rg[kWave + lane];
+    R.Ur = rg[2 * kWave + lane];
+    R.s0 = rg[3 * kWave];
+    R.s1 = rg[3 * kWave + 1];
+    R.s2 = rg[3 * kWave + 2];
+    constexpr int U = 28;  // one batch covers a 28 KiB region
+    for (int32_t base = 0; base < n16; base += U * kWave) {
+        v4i v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int32_t x = base + u * kWave + lane;
+            v[u] = src[x < n16 ? x : n16 - 1];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int32_t x = base + u * kWave + lane;
+            if (x < n16) dst[x] = v[u];
+        }
+    }
+    wsync();
+}
 
 // Grid-wide barrier on a monotonic arrival counter; false if it timed out
 // (then every workgroup stops).  Every thread of the workgroup takes part.
@@ -1263,7 +1333,6 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
                 for (int32_t base = u0; base < u1; base += U * nt) {
                     // every slot loads (clamped to the last unit), so all U
                     // loads are in flight before the first store
-                    typedef int32_t v4i __attribute__((ext_vector_type(4)));
                     v4i v[U];
                     int64_t dsto[U];
 #pragma unroll
@@ -1281,12 +1350,12 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
                 }
             }
             // and the rest of its state from the parent's own slab
-            if (publish) member_store(a, M, g, R);
+            if (publish) member_publish(a, smem + a.lds_shared + (int64_t)wv * a.lds_member, r.blobs + (int64_t)gw * r.blob_bytes, R);
         }
         if (!grid_sync(r.bar, (unsigned)nb * ++epoch, r.err, &s_ok)) return;  // B
         if (resample) {
             if (active && src_slab >= 0)
-                member_load(a, M, tb, slab_ptrs(a, a.slabs + (int64_t)src_slab * a.off.bytes), R);
+                member_receive(a, smem + a.lds_shared + (int64_t)wv * a.lds_member, r.blobs + (int64_t)src_slab * r.blob_bytes, R);
             for (int32_t mm = tid; mm < pop; mm += nt) slab[mm] = slabn[mm];
             __syncthreads();
         }

@@ -161,20 +161,23 @@ int window_stats(const routepack_problem *p, const int32_t *lengths, const int32
     return ROUTEPACK_OK;
 }
 
-int overflow_check(const routepack_problem *p, int64_t n_rows, const WindowStats &ws,
-                   bool w_as_int32) {
-    const long double lim = 9007199254740992.0L;  // 2^53
-    const long double C = (long double)p->capacity;
-    // W bound of a capacity-feasible layout: a row-shard holds at most
-    // maxD * C tokens and q[i][l][p] <= rate * t_i.
+int64_t w_entry_bound(const routepack_problem *p, const WindowStats &ws) {
+    // A row-shard holds at most maxD * C tokens and q[i][l][p] <= rate * t_i.
     int32_t maxd = 0;
     {
         std::vector<int32_t> cnt(p->n_edp, 0);
         for (int d = 0; d < p->n_dp; ++d) cnt[p->dp_to_edp[d]]++;
         for (int g = 0; g < p->n_edp; ++g) maxd = cnt[g] > maxd ? cnt[g] : maxd;
     }
-    const long double wcap = (long double)ws.q_rate * (long double)maxd * C;
-    const int64_t wb = wcap < (long double)ws.w_bound ? (int64_t)wcap : ws.w_bound;
+    const long double wcap = (long double)ws.q_rate * (long double)maxd * (long double)p->capacity;
+    return wcap < (long double)ws.w_bound ? (int64_t)wcap : ws.w_bound;
+}
+
+int overflow_check(const routepack_problem *p, int64_t n_rows, const WindowStats &ws,
+                   bool w_as_int32) {
+    const long double lim = 9007199254740992.0L;  // 2^53
+    const long double C = (long double)p->capacity;
+    const int64_t wb = w_entry_bound(p, ws);
     long double a_max = 0.0L;
     for (int s = 0; s < p->n_stages; ++s)
         a_max += (long double)p->alpha_fp[s] * C + (long double)p->beta_fp[s] * C * C;

@@ -165,6 +165,13 @@ __device__ inline int64_t row_min64(int64_t v) {
     o = dpp64<kDppMirror>(v, v); v = o < v ? o : v;
     return v;
 }
+__device__ inline int32_t row_sum32(int32_t v) {
+    v += dpp32<kDppXor1>(v, 0);
+    v += dpp32<kDppXor2>(v, 0);
+    v += dpp32<kDppHalfMirror>(v, 0);
+    v += dpp32<kDppMirror>(v, 0);
+    return v;
+}
 __device__ inline int64_t row_sum64(int64_t v) {
     v += dpp64<kDppXor1>(v, 0);
     v += dpp64<kDppXor2>(v, 0);

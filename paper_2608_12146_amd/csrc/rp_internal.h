@@ -61,6 +61,8 @@ struct WindowStats {
 };
 int window_stats(const routepack_problem *p, const int32_t *lengths, const int32_t *q,
                  WindowStats *out, hipStream_t stream);
+// Bound of every W entry of a capacity-feasible layout: min(w_bound, q_rate * maxD * C).
+int64_t w_entry_bound(const routepack_problem *p, const WindowStats &ws);
 
 // R * G * (A_max + E_max + 1) < 2^53 and 2^F * C < 2^53 (scores exact in
 // int64 and as doubles), with W bounded by min(w_bound, q_rate * maxD * C)
