@@ -53,6 +53,7 @@ struct AnnealArgs {
     double inv_scale;           // 1 / (2^F C) when it is
     unsigned long long *phase_cycles;  // [pop][8] with RP_PHASE_TIMERS builds, else unused
     const int32_t *qzero;       // [L * P] zeros (chain kernels: the q row of "no sample")
+    const int32_t *qt;          // chain kernels: q rows in chunk-major order [N][P/4][L][4]
     int32_t sum32;              // L * (W entry bound) < 2^31: per-row layer sums fit int32
 };
 
@@ -84,6 +85,10 @@ struct RunArgs {
 // every lane and the score.
 inline int64_t run_blob_bytes(int32_t lds_member) { return ((int64_t)lds_member + 8 * (3 * 64 + 3) + 255) & ~(int64_t)255; }
 
+// Chain kernels: rows of L x P int32 are kept chunk-major, [P/4][L][4], so a
+// 16-byte access of every lane of a half-wave (lane = layer) is contiguous.
+// Rewrites the W rows of every slab in place and writes qt (N rows).
+int chain_prepare(AnnealArgs &a, int32_t *qt, hipStream_t stream);
 // Chain kernel plan and launchers (rp_anneal_chain.hip).
 bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out, int32_t *dv_out);
 int launch_anneal_chain(const AnnealArgs &a, int32_t pv, int32_t dv, hipStream_t stream);

@@ -1119,6 +1119,12 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
         whole = rc == ROUTEPACK_OK;
     }
     const bool chain = chain_fits && !whole && want_chain;
+    if (whole || chain) {
+        a.slabs = slabA;
+        int32_t *qt = scr.get<int32_t>(LP64 > 0 ? (size_t)N * LP64 : 1);
+        if (scr.failed()) return ROUTEPACK_E_DEVICE;
+        RP_TRY(chain_prepare(a, qt, stream));
+    }
     const bool fast = whole || chain || (want_wave && wave_plan(a, n_cu, &mpw, &tlds));
     if (!fast && !want_group) return ROUTEPACK_E_UNSUPPORTED;
     if (prm->level_kernel)

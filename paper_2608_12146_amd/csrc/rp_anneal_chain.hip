@@ -617,17 +617,18 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
     // (half 0) or hb (half 1), the q row that leaves that row-shard (qx) and
     // the one that enters it (qy), so every lane's new row is wr - qx + qy.
     // A relocation moves no sample back: its missing row is the zero row.
+    // Rows are chunk-major ([P/4][L][4]): chunk x of layer ll is int4 x * L + ll.
     auto load_rows = [&](int32_t i, int32_t j, int32_t ha, int32_t hb, int4 *wr, int4 *qx, int4 *qy) {
         const int32_t row = half ? hb : ha, ll = lay_act ? hl : L - 1;
-        const int32_t *qi = a.q + (int64_t)i * a.LP, *qj = j >= 0 ? a.q + (int64_t)j * a.LP : a.qzero;
-        const int4 *wp = reinterpret_cast<const int4 *>(W + ((int64_t)row * L + ll) * PV);
-        const int4 *xp = reinterpret_cast<const int4 *>((half ? qj : qi) + ll * PV);
-        const int4 *yp = reinterpret_cast<const int4 *>((half ? qi : qj) + ll * PV);
+        const int32_t *qi = a.qt + (int64_t)i * a.LP, *qj = j >= 0 ? a.qt + (int64_t)j * a.LP : a.qzero;
+        const int4 *wp = reinterpret_cast<const int4 *>(W + (int64_t)row * a.LP) + ll;
+        const int4 *xp = reinterpret_cast<const int4 *>(half ? qj : qi) + ll;
+        const int4 *yp = reinterpret_cast<const int4 *>(half ? qi : qj) + ll;
 #pragma unroll
         for (int x = 0; x < PV / 4; ++x) {
-            wr[x] = wp[x];
-            qx[x] = xp[x];
-            qy[x] = yp[x];
+            wr[x] = wp[x * L];
+            qx[x] = xp[x * L];
+            qy[x] = yp[x * L];
         }
     };
 
@@ -798,7 +799,14 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                 } else {
                     const double z = delta / temp;
                     const double u = (double)fw7 * (1.0 / 4294967296.0);
-                    accept = u < exp_det(-z);
+                    // u < exp_det(-z), decided without the series when u is
+                    // clear of the bracket 1 - z <= exp(-z) <= 1 - z + z^2/2
+                    // (z >= 0); the 2^-40 margins exceed every rounding error
+                    // of the bounds and of exp_det (a few ulp).
+                    const double omz = 1.0 - z;
+                    if (z < 0.5 && u < omz * (1.0 - 0x1p-40)) accept = true;
+                    else if (z < 0.5 && u >= (omz + (0.5 * z) * z) * (1.0 + 0x1p-40)) accept = false;
+                    else accept = u < exp_det(-z);
                 }
             }
             if (!accept) {
@@ -810,10 +818,10 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
             // ---- commit
             wsync();
             if (two && lay_act) {
-                int4 *wp = reinterpret_cast<int4 *>(W + ((int64_t)(half ? hb : ha) * L + hl) * PV);
+                int4 *wp = reinterpret_cast<int4 *>(W + (int64_t)(half ? hb : ha) * a.LP) + hl;
 #pragma unroll
                 for (int x = 0; x < PV / 4; ++x)
-                    wp[x] = make_int4(nw[4 * x], nw[4 * x + 1], nw[4 * x + 2], nw[4 * x + 3]);
+                    wp[x * L] = make_int4(nw[4 * x], nw[4 * x + 1], nw[4 * x + 2], nw[4 * x + 3]);
             }
             if (!reloc) {
                 if (small) {
@@ -1026,7 +1034,9 @@ __device__ inline bool grid_sync(unsigned *bar, unsigned target, int32_t *err, i
         int32_t good = 1;
         while (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
             __builtin_amdgcn_s_sleep(2);
-            if (++spins > kSpinLimit || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+            // (the error flag is polled every 32 spins: one load per spin)
+            if ((++spins & 31) == 0 &&
+                (spins > kSpinLimit || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))) {
                 __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 good = 0;
                 break;
@@ -1364,6 +1374,39 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
     if (active) member_store(a, M, g, R);
     if (blockIdx.x == 0)
         for (int32_t mm = tid; mm < pop; mm += nt) r.slab_of_out[mm] = slab[mm];
+}
+
+// Rows of L x P int32 from layer-major [L][P] to chunk-major [P/4][L][4],
+// one row per workgroup (in place when src == dst).
+__global__ void __launch_bounds__(256) k_rows_to_chunks(const int32_t *src, int32_t *dst, int64_t n_rows,
+                                                      int64_t row_stride, int64_t rows_per_group,
+                                                      int64_t group_stride, int32_t L, int32_t P) {
+    __shared__ int32_t row[512];  // L * P <= 32 * 16
+    const int64_t rr = blockIdx.x;
+    if (rr >= n_rows) return;
+    const int64_t off = (rr / rows_per_group) * group_stride + (rr % rows_per_group) * row_stride;
+    const int32_t LP = L * P;
+    for (int32_t e = threadIdx.x; e < LP; e += blockDim.x) row[e] = src[off + e];
+    __syncthreads();
+    for (int32_t e = threadIdx.x; e < LP; e += blockDim.x) {
+        const int32_t l = e / P, p = e - l * P;
+        dst[off + ((p >> 2) * L + l) * 4 + (p & 3)] = row[e];
+    }
+}
+
+int chain_prepare(AnnealArgs &a, int32_t *qt, hipStream_t stream) {
+    if (a.L * a.P > 512 || (a.P & 3) != 0) return ROUTEPACK_E_UNSUPPORTED;
+    if (a.LP > 0) {
+        hipLaunchKernelGGL(k_rows_to_chunks, dim3((unsigned)a.N), dim3(256), 0, stream, a.q, qt, (int64_t)a.N,
+                           (int64_t)a.LP, (int64_t)1, (int64_t)a.LP, a.L, a.P);
+        int32_t *w = reinterpret_cast<int32_t *>(a.slabs + a.off.W);
+        const int64_t rows = (int64_t)a.pop * a.RG;
+        hipLaunchKernelGGL(k_rows_to_chunks, dim3((unsigned)rows), dim3(256), 0, stream, w, w, rows, (int64_t)a.LP,
+                           (int64_t)a.RG, a.off.bytes / (int64_t)sizeof(int32_t), a.L, a.P);
+        if (hipGetLastError() != hipSuccess) return ROUTEPACK_E_DEVICE;
+    }
+    a.qt = qt;
+    return ROUTEPACK_OK;
 }
 
 // Launch shape of the chain kernel; false when the problem is outside its
