@@ -117,7 +117,8 @@ def main():
     ap.add_argument("--edp", type=int, default=1, help="EDP shards G (contiguous slot blocks)")
     ap.add_argument("--levels", type=int, default=None, help="levels (default: the window's schedule)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-levels", type=int, default=16, help="levels in the oracle's timed sample")
+    ap.add_argument("--cpu-levels", type=int, default=300,
+                    help="levels in the oracle's timed sample (about 10-30 s on 16 host threads)")
     ap.add_argument("--copy-probe", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
