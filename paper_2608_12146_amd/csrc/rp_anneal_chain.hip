@@ -64,6 +64,13 @@ __device__ inline double energy_k(const AnnealArgs &a, int64_t s0, int64_t s1, i
     return x + 1e-9 * e2;
 }
 
+// energy_k when the scale is known to be a power of two.
+__device__ inline double energy_pow2(const AnnealArgs &a, int64_t s0, int64_t s1, int64_t s2) {
+    const double e0 = (double)s0 * a.inv_scale, e1 = (double)s1 * a.inv_scale, e2 = (double)s2 * a.inv_scale;
+    const double x = e0 + 1e-6 * e1;
+    return x + 1e-9 * e2;
+}
+
 // floor(w m / 2^64) without a branch on the size of m (m varies by lane).
 __device__ inline uint64_t bounded_lane(uint64_t w, uint64_t m) { return __umul64hi(w, m); }
 
@@ -122,13 +129,16 @@ __device__ inline void stage_end(T &...v) {
 
 // Resolves the proposal of this lane against the member's current state.
 // The reads go out in dependent stages; the uniform-mode proposal's reads
-// ride along with the first two stages of the guided chain.
-template <int DV>
+// ride along with the first two stages of the guided chain.  GV == 1 is the
+// common shape compiled for one EDP shard (G == 1), one attention stage
+// (S == 1), 32-bit layer sums, a power-of-two score scale and no step log;
+// GV == 0 takes all of these from the arguments.
+template <int DV, int GV>
 __device__ inline Screen screen(const AnnealArgs &a, const Lds &M, const Tables &tb, uint64_t w0, uint64_t w1,
                                 uint64_t w2, uint64_t w3, uint64_t w4, uint64_t w5, uint64_t w6, int64_t s1,
                                 int64_t s2) {
     Screen sc;
-    const int32_t N = a.N, B = a.B, RG = a.RG, D = a.D, G = a.G;
+    const int32_t N = a.N, B = a.B, RG = a.RG, D = a.D, G = GV == 1 ? 1 : a.G;
     const bool guided = (uint32_t)w0 < a.p_guide;
     const bool reloc = (uint32_t)(w0 >> 32) < a.rho;
     // Uniform-mode samples (and target cell of a relocation) straight from
@@ -592,12 +602,13 @@ struct LevelOut {
     double e;            // terminal energy
 };
 
-template <int PV, int DV>
+template <int PV, int DV, int GV>
 __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const Tables &tb, int32_t *W, int m,
                                         int32_t level, double temp, int64_t x0, int64_t x1, int64_t x2,
-                                        uint8_t *log, int64_t *res, int64_t *trace_row, Regs &R) {
+                                        uint8_t *log_arg, int64_t *res, int64_t *trace_row, Regs &R) {
+    uint8_t *const log = GV == 1 ? nullptr : log_arg;  // (the common shape is launched without a step log)
     const int lane = lane_id();
-    const int32_t N = a.N, B = a.B, RG = a.RG, D = a.D, G = a.G, L = a.L;
+    const int32_t N = a.N, B = a.B, RG = a.RG, D = a.D, G = GV == 1 ? 1 : a.G, L = a.L;
     int64_t Jr = R.Jr, Ar = R.Ar, Ur = R.Ur, s0 = R.s0, s1 = R.s1, s2 = R.s2;
     int64_t b0 = s0, b1 = s1, b2 = s2;
     int32_t best_is_start = 1;
@@ -609,7 +620,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
         best_is_start = 0;
     }
     int64_t n_acc = 0, n_eval = 0;
-    double e_cur = energy_k(a, s0, s1, s2);
+    double e_cur = GV == 1 ? energy_pow2(a, s0, s1, s2) : energy_k(a, s0, s1, s2);
     const int half = lane >> 5, hl = lane & 31, cx = lane & 15;
     const bool lay_act = hl < L;  // lane holds layer hl of row-shard a / b
     const bool cell_lane = (lane & 16) == 0;
@@ -641,7 +652,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
         const uint64_t w0 = b0w.v[0], w1 = b0w.v[1], w2 = b0w.v[2], w3 = b0w.v[3];
         const uint64_t w4 = b1w.v[0], w5 = b1w.v[1], w6 = b1w.v[2], w7 = b1w.v[3];
         uint64_t pending = __ballot(k < a.K);
-        Screen sc = screen<DV>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
+        Screen sc = screen<DV, GV>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
         uint64_t feas = __ballot(sc.feas && k < a.K);
         while (pending) {
             const uint64_t cand = pending & feas;
@@ -717,7 +728,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
             int64_t Arow = 0, cw = 0;
 #pragma unroll
             for (int s = 0; s < kMaxStages; ++s) {
-                if (s < a.S) {
+                if (s < (GV == 1 ? 1 : a.S)) {
                     const int64_t cost = a.alpha[s] * Tc + a.beta[s] * Qc;
                     cw += cact ? cost : 0;
                     Arow = (int64_t)((uint64_t)Arow + (uint64_t)row_max64(cact ? cost : LLONG_MIN));
@@ -741,7 +752,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
 #pragma unroll
                 for (int p = 0; p < PV; ++p) mx = nw[p] > mx ? nw[p] : mx;
                 int64_t suma, sumb;
-                if (a.sum32) {  // L times the W bound fits 31 bits
+                if (GV == 1 || a.sum32) {  // L times the W bound fits 31 bits
                     const int32_t sm = row_sum32(lay_act ? mx : 0);
                     suma = (int64_t)__builtin_amdgcn_readlane(sm, 0) + __builtin_amdgcn_readlane(sm, 16);
                     sumb = (int64_t)__builtin_amdgcn_readlane(sm, 32) + __builtin_amdgcn_readlane(sm, 48);
@@ -789,8 +800,9 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
             } else {
                 n2 = wave_max(lane < RG ? Jn : LLONG_MIN);
             }
-            const double e_new = energy_k(a, n0, n1, n2);
+            const double e_new = GV == 1 ? energy_pow2(a, n0, n1, n2) : energy_k(a, n0, n1, n2);
             bool accept = lex_less(n0, n1, n2, s0, s1, s2);
+            if (!accept && !(e_new > e_cur)) accept = true;  // delta <= 0 (the divisor is >= 1)
             if (!accept) {
                 const double den = fabs(e_cur) > 1.0 ? fabs(e_cur) : 1.0;
                 const double delta = (e_new - e_cur) / den;
@@ -897,7 +909,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                     for (int32_t x = lane; x < N; x += kWave) bl[x] = M.cell[x];
             }
             if (pending) {
-                sc = screen<DV>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
+                sc = screen<DV, GV>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
                 feas = __ballot(sc.feas && k < a.K);
             }
         }
@@ -927,7 +939,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
 
 // One level of every member: state from the member's slab, K proposals,
 // state back to the slab.
-template <int PV, int DV>
+template <int PV, int DV, int GV>
 __global__ void __launch_bounds__(512) k_anneal_chain(AnnealArgs a) {
     extern __shared__ __align__(16) char smem[];
     const Tables tb = load_tables(a, smem);
@@ -938,7 +950,7 @@ __global__ void __launch_bounds__(512) k_anneal_chain(AnnealArgs a) {
     const SlabPtrs g = slab_ptrs(a, a.slabs + (int64_t)a.slab_of[m] * a.off.bytes);
     Regs R;
     member_load(a, M, tb, g, R);
-    member_level<PV, DV>(a, M, tb, g.W, m, a.level, a.temp, a.xscore[0], a.xscore[1], a.xscore[2],
+    member_level<PV, DV, GV>(a, M, tb, g.W, m, a.level, a.temp, a.xscore[0], a.xscore[1], a.xscore[2],
                          a.step_log ? a.step_log + (int64_t)m * a.K : nullptr, a.results + (int64_t)m * kRes,
                          nullptr, R);
     member_store(a, M, g, R);
@@ -1133,7 +1145,7 @@ __device__ inline double wave_min_f64(double v) {
 
 }  // namespace
 
-template <int PV, int DV>
+template <int PV, int DV, int GV>
 __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(AnnealArgs a, RunArgs r) {
     extern __shared__ __align__(16) char smem[];
     __shared__ int64_t s_xs[3], s_k[kRunMaxWaves][4];
@@ -1174,7 +1186,7 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
         int64_t k0 = LLONG_MAX, k1 = LLONG_MAX, k2 = LLONG_MAX, kj = LLONG_MAX;
         double emin = __builtin_inf();
         if (active) {
-            const LevelOut lo = member_level<PV, DV>(
+            const LevelOut lo = member_level<PV, DV, GV>(
                 a, M, tb, g.W, m, level, temp, s_xs[0], s_xs[1], s_xs[2],
                 r.step_log ? r.step_log + ((int64_t)n * pop + m) * K : nullptr, a.results + (int64_t)m * kRes,
                 r.trace ? r.trace + ((int64_t)n * pop + m) * 8 : nullptr, R);
@@ -1450,21 +1462,21 @@ bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out,
     return true;
 }
 
-template <int PV, int DV>
+template <int PV, int DV, int GV>
 static int chain_launch_t(const AnnealArgs &a, hipStream_t stream) {
     const size_t lds = (size_t)a.lds_shared + (size_t)a.mpw * a.lds_member;
-    if (hipFuncSetAttribute((const void *)k_anneal_chain<PV, DV>, hipFuncAttributeMaxDynamicSharedMemorySize,
+    if (hipFuncSetAttribute((const void *)k_anneal_chain<PV, DV, GV>, hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)lds) != hipSuccess)
         return ROUTEPACK_E_DEVICE;
     const unsigned grid = (unsigned)((a.pop + a.mpw - 1) / a.mpw);
-    hipLaunchKernelGGL((k_anneal_chain<PV, DV>), dim3(grid), dim3(kWave * a.mpw), lds, stream, a);
+    hipLaunchKernelGGL((k_anneal_chain<PV, DV, GV>), dim3(grid), dim3(kWave * a.mpw), lds, stream, a);
     return hipGetLastError() == hipSuccess ? ROUTEPACK_OK : ROUTEPACK_E_DEVICE;
 }
 
 // Level-end tables of the whole-schedule kernel (after the member regions).
 static int64_t run_lend_bytes(int32_t pop) { return 28 * (int64_t)pop; }
 
-template <int PV, int DV>
+template <int PV, int DV, int GV>
 static int chain_run_t(const AnnealArgs &a, const RunArgs &r0, int32_t n_cu, bool launch, hipStream_t stream) {
     RunArgs r = r0;
     if (a.mpw > kRunMaxWaves) return ROUTEPACK_E_UNSUPPORTED;
@@ -1473,7 +1485,7 @@ static int chain_run_t(const AnnealArgs &a, const RunArgs &r0, int32_t n_cu, boo
     // static LDS of the kernel is below 1 KiB
     if (lds + 1024 > 160 * 1024) return ROUTEPACK_E_UNSUPPORTED;
     r.o_lend = (int32_t)o_lend;
-    const void *fn = (const void *)k_anneal_chain_run<PV, DV>;
+    const void *fn = (const void *)k_anneal_chain_run<PV, DV, GV>;
     if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
         return ROUTEPACK_E_DEVICE;
     const int grid = (a.pop + a.mpw - 1) / a.mpw, block = kWave * a.mpw;
@@ -1493,34 +1505,36 @@ static int chain_run_t(const AnnealArgs &a, const RunArgs &r0, int32_t n_cu, boo
 // kernel; ROUTEPACK_E_UNSUPPORTED when its workgroups cannot all be resident.
 int chain_run(const AnnealArgs &a, const RunArgs &r, int32_t pv, int32_t dv, int32_t n_cu, bool launch,
               hipStream_t stream) {
+    const bool g1 = a.G == 1 && a.S == 1 && a.sum32 && a.scale_pow2 && !r.step_log;  // the common shape
     if (dv == 8) {
         switch (pv) {
-            case 4: return chain_run_t<4, 8>(a, r, n_cu, launch, stream);
-            case 8: return chain_run_t<8, 8>(a, r, n_cu, launch, stream);
-            case 16: return chain_run_t<16, 8>(a, r, n_cu, launch, stream);
+            case 4: return g1 ? chain_run_t<4, 8, 1>(a, r, n_cu, launch, stream) : chain_run_t<4, 8, 0>(a, r, n_cu, launch, stream);
+            case 8: return g1 ? chain_run_t<8, 8, 1>(a, r, n_cu, launch, stream) : chain_run_t<8, 8, 0>(a, r, n_cu, launch, stream);
+            case 16: return g1 ? chain_run_t<16, 8, 1>(a, r, n_cu, launch, stream) : chain_run_t<16, 8, 0>(a, r, n_cu, launch, stream);
         }
     } else {
         switch (pv) {
-            case 4: return chain_run_t<4, 16>(a, r, n_cu, launch, stream);
-            case 8: return chain_run_t<8, 16>(a, r, n_cu, launch, stream);
-            case 16: return chain_run_t<16, 16>(a, r, n_cu, launch, stream);
+            case 4: return g1 ? chain_run_t<4, 16, 1>(a, r, n_cu, launch, stream) : chain_run_t<4, 16, 0>(a, r, n_cu, launch, stream);
+            case 8: return g1 ? chain_run_t<8, 16, 1>(a, r, n_cu, launch, stream) : chain_run_t<8, 16, 0>(a, r, n_cu, launch, stream);
+            case 16: return g1 ? chain_run_t<16, 16, 1>(a, r, n_cu, launch, stream) : chain_run_t<16, 16, 0>(a, r, n_cu, launch, stream);
         }
     }
     return ROUTEPACK_E_UNSUPPORTED;
 }
 
 int launch_anneal_chain(const AnnealArgs &a, int32_t pv, int32_t dv, hipStream_t stream) {
+    const bool g1 = a.G == 1 && a.S == 1 && a.sum32 && a.scale_pow2 && !a.step_log;  // the common shape
     if (dv == 8) {
         switch (pv) {
-            case 4: return chain_launch_t<4, 8>(a, stream);
-            case 8: return chain_launch_t<8, 8>(a, stream);
-            case 16: return chain_launch_t<16, 8>(a, stream);
+            case 4: return g1 ? chain_launch_t<4, 8, 1>(a, stream) : chain_launch_t<4, 8, 0>(a, stream);
+            case 8: return g1 ? chain_launch_t<8, 8, 1>(a, stream) : chain_launch_t<8, 8, 0>(a, stream);
+            case 16: return g1 ? chain_launch_t<16, 8, 1>(a, stream) : chain_launch_t<16, 8, 0>(a, stream);
         }
     } else {
         switch (pv) {
-            case 4: return chain_launch_t<4, 16>(a, stream);
-            case 8: return chain_launch_t<8, 16>(a, stream);
-            case 16: return chain_launch_t<16, 16>(a, stream);
+            case 4: return g1 ? chain_launch_t<4, 16, 1>(a, stream) : chain_launch_t<4, 16, 0>(a, stream);
+            case 8: return g1 ? chain_launch_t<8, 16, 1>(a, stream) : chain_launch_t<8, 16, 0>(a, stream);
+            case 16: return g1 ? chain_launch_t<16, 16, 1>(a, stream) : chain_launch_t<16, 16, 0>(a, stream);
         }
     }
     return ROUTEPACK_E_UNSUPPORTED;
