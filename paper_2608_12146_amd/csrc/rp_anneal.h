@@ -48,6 +48,7 @@ struct AnnealArgs {
     int32_t o_cell, o_pool, o_start, o_T, o_Q, o_acost, o_Jpre;
     int32_t o_Jpiv, o_tshared;  // chain kernel: J pivots (per member), lengths table (shared)
     uint32_t ginv, dinv;        // chain kernel: ceil(2^32 / G), ceil(2^32 / D) (unused when G, D == 1)
+    int32_t dshift;             // chain kernel: log2 D when D is a power of two, else -1
     int32_t dv, o_hcnt, o_hcell;  // chain kernel: cost-prefix stride; row-shard slot tables (shared)
     int32_t scale_pow2;         // 2^F C is a power of two
     double inv_scale;           // 1 / (2^F C) when it is

@@ -130,9 +130,9 @@ __device__ inline void stage_end(T &...v) {
 // Resolves the proposal of this lane against the member's current state.
 // The reads go out in dependent stages; the uniform-mode proposal's reads
 // ride along with the first two stages of the guided chain.  GV == 1 is the
-// common shape compiled for one EDP shard (G == 1), one attention stage
-// (S == 1), 32-bit layer sums, a power-of-two score scale and no step log;
-// GV == 0 takes all of these from the arguments.
+// common shape compiled for one EDP shard (G == 1) with a power-of-two slot
+// count D, one attention stage (S == 1), 32-bit layer sums, a power-of-two
+// score scale and no step log; GV == 0 takes all of these from the arguments.
 template <int DV, int GV>
 __device__ inline Screen screen(const AnnealArgs &a, const Lds &M, const Tables &tb, uint64_t w0, uint64_t w1,
                                 uint64_t w2, uint64_t w3, uint64_t w4, uint64_t w5, uint64_t w6, int64_t s1,
@@ -675,7 +675,8 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
             const uint32_t fw7 = __builtin_amdgcn_readlane((int32_t)(uint32_t)(w7 >> 32), f);
             const bool reloc = fw0 < a.rho;
             n_eval += 1;
-            const int32_t ra = div_small(c1, D, a.dinv), rb = div_small(c2, D, a.dinv);
+            const int32_t ra = GV == 1 ? c1 >> a.dshift : div_small(c1, D, a.dinv);
+            const int32_t rb = GV == 1 ? c2 >> a.dshift : div_small(c2, D, a.dinv);
             const int32_t ga = G == 1 ? 0 : tb.shard[c1 - ra * D], gb = G == 1 ? 0 : tb.shard[c2 - rb * D];
             const int32_t ha = ra * G + ga, hb = rb * G + gb;
             const bool two = ha != hb;
@@ -1443,6 +1444,9 @@ bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out,
     a.o_Jpiv = a.o_Jpre + 8 * 128;
     a.ginv = (uint32_t)((((uint64_t)1 << 32) + (uint64_t)a.G - 1) / (uint64_t)a.G);
     a.dinv = (uint32_t)((((uint64_t)1 << 32) + (uint64_t)a.D - 1) / (uint64_t)a.D);
+    a.dshift = -1;
+    for (int32_t sh = 0; sh < 16; ++sh)
+        if ((1 << sh) == a.D) a.dshift = sh;
     const int64_t member = o;
     int64_t tab = up16(4 * ((int64_t)a.G * a.D + 2 * a.G + a.D));
     a.o_hcnt = (int32_t)tab; tab = up16(tab + 4 * (int64_t)a.RG);
@@ -1505,7 +1509,7 @@ static int chain_run_t(const AnnealArgs &a, const RunArgs &r0, int32_t n_cu, boo
 // kernel; ROUTEPACK_E_UNSUPPORTED when its workgroups cannot all be resident.
 int chain_run(const AnnealArgs &a, const RunArgs &r, int32_t pv, int32_t dv, int32_t n_cu, bool launch,
               hipStream_t stream) {
-    const bool g1 = a.G == 1 && a.S == 1 && a.sum32 && a.scale_pow2 && !r.step_log;  // the common shape
+    const bool g1 = a.G == 1 && a.dshift >= 0 && a.S == 1 && a.sum32 && a.scale_pow2 && !r.step_log;  // the common shape
     if (dv == 8) {
         switch (pv) {
             case 4: return g1 ? chain_run_t<4, 8, 1>(a, r, n_cu, launch, stream) : chain_run_t<4, 8, 0>(a, r, n_cu, launch, stream);
@@ -1523,7 +1527,7 @@ int chain_run(const AnnealArgs &a, const RunArgs &r, int32_t pv, int32_t dv, int
 }
 
 int launch_anneal_chain(const AnnealArgs &a, int32_t pv, int32_t dv, hipStream_t stream) {
-    const bool g1 = a.G == 1 && a.S == 1 && a.sum32 && a.scale_pow2 && !a.step_log;  // the common shape
+    const bool g1 = a.G == 1 && a.dshift >= 0 && a.S == 1 && a.sum32 && a.scale_pow2 && !a.step_log;  // the common shape
     if (dv == 8) {
         switch (pv) {
             case 4: return g1 ? chain_launch_t<4, 8, 1>(a, stream) : chain_launch_t<4, 8, 0>(a, stream);
