@@ -90,6 +90,10 @@ struct Tables {
 struct Screen {
     int32_t i, j, c1, c2, pos_i, pos_j, ti, tj;
     bool feas;
+    // guided picks: source and target row-shards and the prefix entries
+    // that bound each pick (J_pre[h1 - 1], J_pre[h1], V_pre[h4 - 1], V_pre[h4])
+    int32_t h1, h4;
+    int64_t jlo, jhi, vlo, vhi;
 };
 
 __device__ inline int32_t clamp0(int32_t v, int32_t hi) { return v < 0 ? 0 : (v > hi ? hi : v); }
@@ -200,7 +204,15 @@ __device__ inline Screen screen(const AnnealArgs &a, const Lds &M, const Tables 
     for (int x = 0; x < DV; ++x) cv[x] = M.Cp[h1 * DV + x];
     int64_t tot = M.Ctot[h1];
     int32_t cnt1 = tb.hcnt[h1], cnt2 = tb.hcnt[h4];
-    stage_end(tot, cnt1, cnt2);
+    int64_t jlo = M.Jpre[h1 > 0 ? h1 - 1 : 0], jhi = M.Jpre[h1];
+    int64_t vlo = M.Vpre[h4 > 0 ? h4 - 1 : 0], vhi = M.Vpre[h4];
+    stage_end(tot, cnt1, cnt2, jlo, jhi, vlo, vhi);
+    sc.h1 = h1;
+    sc.h4 = h4;
+    sc.jlo = h1 > 0 ? jlo : 0;
+    sc.jhi = jhi;
+    sc.vlo = h4 > 0 ? vlo : 0;
+    sc.vhi = vhi;
 #pragma unroll
     for (int x = 0; x < DV; ++x) stage_end(cv[x]);
     int32_t xi;
@@ -654,8 +666,20 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
         uint64_t pending = __ballot(k < a.K);
         Screen sc = screen<DV, GV>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
         uint64_t feas = __ballot(sc.feas && k < a.K);
+        uint64_t valid = ~0ull;  // lanes whose screen is current
         while (pending) {
-            const uint64_t cand = pending & feas;
+            uint64_t cand = pending & feas;
+            {
+                // The next candidate and every pending lane below it must be
+                // current; otherwise screen the batch again.
+                const uint64_t stale = pending & ~valid;
+                if (stale && (!cand || (stale & (~stale + 1)) <= (cand & (~cand + 1)))) {
+                    sc = screen<DV, GV>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
+                    feas = __ballot(sc.feas && k < a.K);
+                    valid = ~0ull;
+                    cand = pending & feas;
+                }
+            }
             const uint64_t below = cand ? (cand & (~cand + 1)) - 1 : ~0ull;
             if (log && ((pending & below) >> lane) & 1ull) log[k] = 0;
             if (!cand) break;
@@ -895,6 +919,35 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                 Ar = Ab;
             }
             write_jpre(M, Jr, RG, n2);
+            if (pending) {
+                // A screen stays current unless the move touched what it
+                // read: its cells (lengths, members, sizes), the cell costs
+                // of its source row-shard, or the prefix interval holding
+                // one of its picks.  A pick keeps its row-shard when it lies
+                // in the interval after the move's J deltas; V_pre moves by
+                // (h + 1)(n2 - s2) besides.  A relocation shifts the members
+                // of the cells strictly between its two cells by one place.
+                auto shift = [&](int32_t h) -> int64_t { return (h >= ha ? dJa : 0) + (h >= hb ? dJb : 0); };
+                const int64_t ds2 = n2 - s2;
+                sc.jlo += shift(sc.h1 - 1);
+                sc.jhi += shift(sc.h1);
+                sc.vlo += (int64_t)sc.h4 * ds2 - shift(sc.h4 - 1);
+                sc.vhi += (int64_t)(sc.h4 + 1) * ds2 - shift(sc.h4);
+                bool keep = sc.c1 != c1 && sc.c1 != c2 && sc.c2 != c1 && sc.c2 != c2;
+                if ((uint32_t)w0 < a.p_guide) {
+                    const uint64_t pk1 = bounded_uniform(w1, (uint64_t)n1);
+                    const uint64_t pk4 = bounded_uniform(w4, (uint64_t)((int64_t)RG * (n2 + 1) - n1));
+                    keep = keep && sc.h1 != ha && sc.h1 != hb && (uint64_t)sc.jlo <= pk1 &&
+                           pk1 < (uint64_t)sc.jhi && (uint64_t)sc.vlo <= pk4 && pk4 < (uint64_t)sc.vhi;
+                }
+                if (reloc) {
+                    const int32_t lo = c1 < c2 ? c1 : c2, hi = c1 < c2 ? c2 : c1, d = c1 < c2 ? -1 : 1;
+                    if (sc.pos_i >= 0 && sc.c1 > lo && sc.c1 < hi) sc.pos_i += d;
+                    if (sc.pos_j >= 0 && sc.c2 > lo && sc.c2 < hi) sc.pos_j += d;
+                }
+                // (screens drawn while s1 was 0 picked h1 uniformly)
+                valid = s1 > 0 && n1 > 0 ? valid & __ballot(keep) : 0;
+            }
             Ur = Un;
             s0 = n0;
             s1 = n1;
@@ -908,10 +961,6 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                 best_is_start = 0;
                 if (lex_less(s0, s1, s2, x0, x1, x2))
                     for (int32_t x = lane; x < N; x += kWave) bl[x] = M.cell[x];
-            }
-            if (pending) {
-                sc = screen<DV, GV>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
-                feas = __ballot(sc.feas && k < a.K);
             }
         }
     }
