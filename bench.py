@@ -50,6 +50,10 @@ def pmc_file(kernel, window):
     return os.path.join(ROOT, "profiles", f"anneal_{kernel}_{window}_pmc.txt")
 
 
+def lds_file(kernel, window):
+    return os.path.join(ROOT, "profiles", f"anneal_{kernel}_{window}_lds.txt")
+
+
 def _code_text(src: str) -> str:
     """The source with // comments and blank lines removed (comment edits do
     not change the kernel the counters were taken on)."""
@@ -72,9 +76,8 @@ def kernel_source_hash(kernel) -> str:
     return h.hexdigest()[:16]
 
 
-def read_pmc(kernel, window):
-    """Counter-derived HBM traffic per dispatch, if taken on this kernel's sources."""
-    path = pmc_file(kernel, window)
+def _read_profile(path, kernel):
+    """key: value lines of a counter summary, if taken on this kernel's sources."""
     if not os.path.exists(path):
         return None
     kv = {}
@@ -84,9 +87,35 @@ def read_pmc(kernel, window):
             kv[k.strip()] = v.strip()
     if kv.get("kernel_source_sha256_16") != kernel_source_hash(kernel):
         return None
+    return kv
+
+
+def read_pmc(kernel, window):
+    """Counter-derived HBM traffic per dispatch, if taken on this kernel's sources."""
+    kv = _read_profile(pmc_file(kernel, window), kernel)
     try:
-        return float(kv["hbm_bytes_per_dispatch"])
+        return float(kv["hbm_bytes_per_dispatch"]) if kv else None
     except (KeyError, ValueError):
+        return None
+
+
+def read_lds(kernel, window, launch_ms):
+    """LDS bytes per dispatch from the counters (if taken on this kernel's
+    sources) over the live launch time, against the LDS peak (256 B per clock
+    per CU, as the counters show, at 2.4 GHz); the LDS probe's sustained rate
+    rides along."""
+    kv = _read_profile(lds_file(kernel, window), kernel)
+    if not kv:
+        return None
+    try:
+        nbytes = float(kv["lds_load_bytes_per_dispatch"]) + float(kv["lds_store_bytes_per_dispatch"])
+        peak = float(kv["lds_read_peak_gbs"])
+        achieved = nbytes / (launch_ms * 1e6)
+        return {"achieved": achieved, "peak": peak, "unit": "GB/s", "frac": achieved / peak,
+                "bytes_per_launch": nbytes, "probe_gbs": float(kv["lds_probe_gbs"]),
+                "busy_frac": float(kv["lds_busy_frac"]),
+                "bank_conflict_cycles_frac": float(kv["lds_bank_conflict_frac"])}
+    except (KeyError, ValueError, ZeroDivisionError):
         return None
 
 
@@ -108,6 +137,30 @@ def copy_probe():
     print(json.dumps({"copy_probe_bytes": n, "dispatches": 5}))
 
 
+def lds_probe():
+    """LDS read bandwidth of this device: four launches of the library's LDS
+    streaming probe (the first a warm-up); the fastest timed one is reported."""
+    import paper_2608_12146_amd as rp
+    rp.probe_lds_read(256, 64)
+    runs = [rp.probe_lds_read() for _ in range(3)]
+    nbytes, ms = min(runs, key=lambda r: r[1])
+    print(json.dumps({"lds_probe_bytes": nbytes, "ms": ms, "GB/s": nbytes / ms / 1e6, "dispatches": 4}))
+
+
+def occupancy(kernel, pop):
+    """Launch shape of the level kernel at this population on the 256 CUs
+    (1024 SIMDs): the chain kernels run one wave per member and spread the
+    members over the CUs, at most four per workgroup (the member state fills
+    the LDS)."""
+    if kernel in ("chain_run", "chain"):
+        mpw = max(1, min(4, -(-pop // 256)))  # members per workgroup
+        wgs = -(-pop // mpw)
+        per_cu = -(-wgs // 256)
+        return {"workgroups": wgs, "waves_per_workgroup": mpw, "workgroups_per_cu": per_cu,
+                "waves_per_simd": -(-(mpw * per_cu) // 4), "waves_per_member": 1}
+    return None
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -120,6 +173,7 @@ def main():
     ap.add_argument("--cpu-levels", type=int, default=300,
                     help="levels in the oracle's timed sample (about 10-30 s on 16 host threads)")
     ap.add_argument("--copy-probe", action="store_true")
+    ap.add_argument("--lds-probe", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the planner path is "
@@ -131,6 +185,9 @@ def main():
         sys.exit(1)
     if args.copy_probe:
         copy_probe()
+        return
+    if args.lds_probe:
+        lds_probe()
         return
 
     import paper_2608_12146_amd as rp
@@ -191,6 +248,7 @@ def main():
     launches = args.steps * (1 if level_kernel == "chain_run" else levels)
     achieved = evals * bytes_per_eval / k_sec / 1e9
     traffic = read_pmc(level_kernel, args.window)
+    lds = read_lds(level_kernel, args.window, float(kms.sum()) / launches)
 
     # Objective == oracle: the oracle rescoring of the GPU's x*, the oracle's
     # seed population, and one level of three members recomputed by the oracle.
@@ -244,7 +302,8 @@ def main():
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": "k_anneal_" + level_kernel, "avg_launch_ms": float(kms.sum()) / launches,
                      "launches": launches, "bytes_per_eval": bytes_per_eval,
-                     "algorithmic_bytes_per_launch": evals * bytes_per_eval / launches},
+                     "algorithmic_bytes_per_launch": evals * bytes_per_eval / launches,
+                     "lds": lds, "occupancy": occupancy(level_kernel, w.pop)},
         "cpu_baseline": cpu,
         "attempted_per_s": attempted / dt,
         "evals_per_step": evals // args.steps,

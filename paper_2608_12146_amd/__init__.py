@@ -24,6 +24,8 @@ LEVEL_KERNELS = {0: "workgroup", 1: "wave", 2: "chain", 3: "chain_run"}
 
 EXPORTS = ("routepack_aggregate_demand", "routepack_place_experts", "routepack_pack_rows",
            "routepack_anneal", "routepack_eval_objective", "routepack_strerror")
+# measurement aid declared in include/routepack_probe.h (not part of the method)
+PROBE_EXPORTS = ("routepack_probe_lds_read",)
 
 
 class RoutepackError(RuntimeError):
@@ -67,6 +69,8 @@ def load_library():
         lib.routepack_anneal.argtypes = [P, vp, vp, i32, i32, vp, C.POINTER(_AnnealParams), vp, vp,
                                          vp, vp, vp, vp]
         lib.routepack_eval_objective.argtypes = [P, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp]
+        lib.routepack_probe_lds_read.argtypes = [i32, i32, vp, C.POINTER(C.c_double), C.POINTER(C.c_int64), vp]
+        lib.routepack_probe_lds_read.restype = C.c_int
         lib.routepack_strerror.argtypes = [C.c_int]
         lib.routepack_strerror.restype = C.c_char_p
         for f in EXPORTS:
@@ -230,3 +234,16 @@ def eval_objective(prob: Problem, lengths, q, n_rows, layouts, rank_load=None, w
                                       _ptr(J), _ptr(dg), _ptr(rl), _stream())
     _check("routepack_eval_objective", rc)
     return dict(scores=sc, status=st, J=J, diag=dg)
+
+
+def probe_lds_read(n_workgroups=2048, reps=8192):
+    """LDS read bandwidth of this device (routepack_probe_lds_read): returns
+    (bytes read, launch ms).  A measurement aid, not part of the method."""
+    torch = _torch()
+    lib = load_library()
+    sink = torch.empty(n_workgroups * 256, dtype=torch.int32, device="cuda")
+    ms, nbytes = C.c_double(0.0), C.c_int64(0)
+    _check("routepack_probe_lds_read",
+           lib.routepack_probe_lds_read(int(n_workgroups), int(reps), _ptr(sink), C.byref(ms), C.byref(nbytes),
+                                        _stream()))
+    return int(nbytes.value), float(ms.value)

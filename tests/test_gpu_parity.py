@@ -369,3 +369,29 @@ def test_anneal_error_paths():
         rp.anneal(prob, w.lengths, q, pr["r_star"], pr["population"], [1e-3], 8, 1,
                   best_layout=pr["population"][0], best_score=np.array([1, 2, 3]))
     assert ei.value.code == -4
+
+
+@gpu
+def test_lds_probe_reads_what_it_claims():
+    """The LDS read probe (a measurement aid): the byte count it reports, and
+    the wrapped 64-bit sum of what each thread read (folded to 32 bits) equal
+    to the same sum on the host."""
+    import ctypes as C
+
+    import torch
+    rp = _rp()
+    lib = rp.load_library()
+    nwg, reps = 3, 4099          # reps not a multiple of the 16-step period
+    sink = torch.zeros(nwg * 256, dtype=torch.int32, device="cuda")
+    ms, nb = C.c_double(0.0), C.c_int64(0)
+    _log(f"lds probe {nwg} workgroups x {reps} steps")
+    rc = lib.routepack_probe_lds_read(nwg, reps, C.c_void_p(sink.data_ptr()), C.byref(ms), C.byref(nb),
+                                      C.c_void_p(torch.cuda.current_stream().cuda_stream))
+    assert rc == 0 and nb.value == nwg * 256 * reps * 16 and ms.value > 0.0
+    t = np.arange(256, dtype=np.int64)[:, None]
+    x = ((t + 256 * np.arange(reps, dtype=np.int64)[None, :]) & 4095).astype(np.uint64)
+    k1, k2 = np.array([0x9E3779B97F4A7C15, 0xC2B2AE3D27D4EB4F], dtype=np.uint64)
+    total = (x * k1 + x * k2).sum(axis=1, dtype=np.uint64)   # wraps mod 2^64
+    want = (total ^ (total >> np.uint64(32))).astype(np.uint32)
+    got = sink.cpu().numpy().view(np.uint32).reshape(nwg, 256)
+    assert np.array_equal(got, np.broadcast_to(want, (nwg, 256)))

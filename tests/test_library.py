@@ -11,8 +11,8 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def _declared():
-    src = open(os.path.join(ROOT, "include", "routepack.h")).read()
+def _declared(header="routepack.h"):
+    src = open(os.path.join(ROOT, "include", header)).read()
     return sorted(set(re.findall(r"^(?:int|const char \*)\s*(routepack_\w+)\s*\(", src, re.M)))
 
 
@@ -25,9 +25,23 @@ def test_header_declares_the_boundary():
 def test_library_exports_every_declared_symbol():
     import paper_2608_12146_amd as rp
     lib = rp.load_library()
-    for name in _declared():
-        assert hasattr(lib, name), name
+    headers = sorted(f for f in os.listdir(os.path.join(ROOT, "include")) if f.endswith(".h"))
+    assert headers == ["routepack.h", "routepack_probe.h"]
+    for h in headers:
+        for name in _declared(h):
+            assert hasattr(lib, name), name
+    assert _declared("routepack_probe.h") == list(rp.PROBE_EXPORTS)
     assert lib.routepack_strerror(-5) == b"fixed-point score bound exceeds 2^53"
+
+
+def test_lds_probe_rejects_bad_arguments_without_device_work():
+    import paper_2608_12146_amd as rp
+    lib = rp.load_library()
+    ms, nb = C.c_double(0.0), C.c_int64(0)
+    assert lib.routepack_probe_lds_read(0, 1, C.c_void_p(16), C.byref(ms), C.byref(nb), None) == -1
+    assert lib.routepack_probe_lds_read(1, 0, C.c_void_p(16), C.byref(ms), C.byref(nb), None) == -1
+    assert lib.routepack_probe_lds_read(1, 1, None, C.byref(ms), C.byref(nb), None) == -1
+    assert lib.routepack_probe_lds_read(1 << 30, 1 << 30, C.c_void_p(16), C.byref(ms), C.byref(nb), None) == -1
 
 
 def test_invalid_problems_rejected_without_device_work():
