@@ -48,7 +48,10 @@ struct Lds {
     uint16_t *cell, *pool, *start;
     int32_t *T;
     int64_t *Q;
-    int64_t *Cp;    // [RG][DV] prefix of the cell costs of each row-shard, slot order; kInf past its slots
+    // [RG][DV + 1] prefix of the cell costs of each row-shard, slot order;
+    // kInf past its slots.  The odd row stride (in 8-byte words) spreads the
+    // rows of a wave's random row reads over the LDS banks.
+    int64_t *Cp;
     int64_t *Ctot;  // [RG] total cell cost of each row-shard
     int64_t *Jpre, *Vpre;  // [64] prefixes of the source and target roulette weights (kInf past RG)
     int64_t *Jpiv, *Vpiv;  // [8] their entries 8k+7
@@ -201,7 +204,7 @@ __device__ inline Screen screen(const AnnealArgs &a, const Lds &M, const Tables 
     // padded with kInf past its slots); target cell uniform over its slots
     int64_t cv[DV];
 #pragma unroll
-    for (int x = 0; x < DV; ++x) cv[x] = M.Cp[h1 * DV + x];
+    for (int x = 0; x < DV; ++x) cv[x] = M.Cp[h1 * (DV + 1) + x];
     int64_t tot = M.Ctot[h1];
     int32_t cnt1 = tb.hcnt[h1], cnt2 = tb.hcnt[h4];
     int64_t jlo = M.Jpre[h1 > 0 ? h1 - 1 : 0], jhi = M.Jpre[h1];
@@ -476,7 +479,7 @@ __device__ inline Lds member_lds(const AnnealArgs &a, char *smem, int wv) {
     M.T = reinterpret_cast<int32_t *>(mine + a.o_T);
     M.Q = reinterpret_cast<int64_t *>(mine + a.o_Q);
     M.Cp = reinterpret_cast<int64_t *>(mine + a.o_acost);
-    M.Ctot = M.Cp + a.RG * a.dv;
+    M.Ctot = M.Cp + a.RG * (a.dv + 1);
     M.Jpre = reinterpret_cast<int64_t *>(mine + a.o_Jpre);
     M.Vpre = M.Jpre + 64;
     M.Jpiv = M.Jpre + 128;
@@ -549,7 +552,7 @@ __device__ inline void member_load(const AnnealArgs &a, const Lds &M, const Tabl
     if (lane < RG) {
         const int32_t cnt = tb.hcnt[lane];
         int64_t acc = 0;
-        int64_t *cp = M.Cp + lane * a.dv;
+        int64_t *cp = M.Cp + lane * (a.dv + 1);
         for (int32_t x = 0; x < a.dv; ++x) {
             if (x < cnt) {
                 const int32_t c = tb.hcell[lane * a.dv + x];
@@ -908,7 +911,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
             }
             {
                 const int64_t incl = row_incl_scan64(cw);
-                if (cact) M.Cp[hsel * DV + cx] = incl;
+                if (cact) M.Cp[hsel * (DV + 1) + cx] = incl;
                 if (cact && cx == cnt - 1) M.Ctot[hsel] = incl;
             }
             if (lane == ha) {
@@ -1488,7 +1491,7 @@ bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out,
     a.o_T = (int32_t)o; o = up16(o + 4 * (int64_t)a.B);
     a.o_Q = (int32_t)o; o = up16(o + 8 * (int64_t)a.B);
     a.dv = dv;
-    a.o_acost = (int32_t)o; o = up16(o + 8 * ((int64_t)a.RG * dv + a.RG));  // cost prefixes and totals
+    a.o_acost = (int32_t)o; o = up16(o + 8 * ((int64_t)a.RG * (dv + 1) + a.RG));  // cost prefixes and totals
     a.o_Jpre = (int32_t)o; o = up16(o + 8 * (64 + 64 + 8 + 8));  // J_pre, V_pre and their pivots
     a.o_Jpiv = a.o_Jpre + 8 * 128;
     a.ginv = (uint32_t)((((uint64_t)1 << 32) + (uint64_t)a.G - 1) / (uint64_t)a.G);
