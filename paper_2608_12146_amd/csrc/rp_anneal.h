@@ -49,6 +49,7 @@ struct AnnealArgs {
     int32_t o_Jpiv, o_tshared;  // chain kernel: J pivots (per member), lengths table (shared)
     uint32_t ginv, dinv;        // chain kernel: ceil(2^32 / G), ceil(2^32 / D) (unused when G, D == 1)
     int32_t dshift;             // chain kernel: log2 D when D is a power of two, else -1
+    int32_t rv;                 // chain kernel: row-shards per lane (1 up to 64 row-shards, 2 up to 128)
     int32_t dv, o_hcnt, o_hcell;  // chain kernel: cost-prefix stride; row-shard slot tables (shared)
     int32_t scale_pow2;         // 2^F C is a power of two
     double inv_scale;           // 1 / (2^F C) when it is
@@ -83,8 +84,8 @@ struct RunArgs {
 };
 
 // Bytes of one hand-over image: the member's LDS region, then J, A and U of
-// every lane and the score.
-inline int64_t run_blob_bytes(int32_t lds_member) { return ((int64_t)lds_member + 8 * (3 * 64 + 3) + 255) & ~(int64_t)255; }
+// every lane, the score, and J and A of the lanes' second row-shards.
+inline int64_t run_blob_bytes(int32_t lds_member) { return ((int64_t)lds_member + 8 * (5 * 64 + 3) + 255) & ~(int64_t)255; }
 
 // Chain kernels: rows of L x P int32 are kept chunk-major, [P/4][L][4], so a
 // 16-byte access of every lane of a half-wave (lane = layer) is contiguous.

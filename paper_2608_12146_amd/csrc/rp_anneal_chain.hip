@@ -53,8 +53,8 @@ struct Lds {
     // rows of a wave's random row reads over the LDS banks.
     int64_t *Cp;
     int64_t *Ctot;  // [RG] total cell cost of each row-shard
-    int64_t *Jpre, *Vpre;  // [64] prefixes of the source and target roulette weights (kInf past RG)
-    int64_t *Jpiv, *Vpiv;  // [8] their entries 8k+7
+    int64_t *Jpre, *Vpre;  // [64 RV] prefixes of the source and target roulette weights (kInf past RG)
+    int64_t *Jpiv, *Vpiv;  // [8 RV] their entries 8k+7
 };
 
 // Energy of a score (Eq. pa-energy); when the scale 2^F C is a power of two
@@ -140,7 +140,8 @@ __device__ inline void stage_end(T &...v) {
 // common shape compiled for one EDP shard (G == 1) with a power-of-two slot
 // count D, one attention stage (S == 1), 32-bit layer sums, a power-of-two
 // score scale and no step log; GV == 0 takes all of these from the arguments.
-template <int DV, int GV>
+// RV is the number of row-shards per lane (2 for 65 to 128 row-shards).
+template <int DV, int GV, int RV>
 __device__ inline Screen screen(const AnnealArgs &a, const Lds &M, const Tables &tb, uint64_t w0, uint64_t w1,
                                 uint64_t w2, uint64_t w3, uint64_t w4, uint64_t w5, uint64_t w6, int64_t s1,
                                 int64_t s2) {
@@ -160,24 +161,26 @@ __device__ inline Screen screen(const AnnealArgs &a, const Lds &M, const Tables 
     const uint64_t pk1 = bounded_uniform(w1, (uint64_t)s1);
     const uint64_t pk4 = bounded_uniform(w4, (uint64_t)((int64_t)RG * (s2 + 1) - s1));
     // stage 1: pivots; the uniform-mode cells and lengths
-    int64_t jp[8], vp[8];
+    constexpr int NP = 8 * RV;
+    int64_t jp[NP], vp[NP];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
+    for (int k = 0; k < NP; ++k) {
         jp[k] = M.Jpiv[k];
         vp[k] = M.Vpiv[k];
     }
     int32_t cir = M.cell[ir], cjr = M.cell[jr];
     int32_t tir = tb.t[ir], tjr = tb.t[jr];
-    stage_end(jp[0], jp[1], jp[2], jp[3], jp[4], jp[5], jp[6], jp[7], vp[0], vp[1], vp[2], vp[3], vp[4], vp[5],
-              vp[6], vp[7], cir, cjr, tir, tjr);
+#pragma unroll
+    for (int k = 0; k < NP; ++k) stage_end(jp[k], vp[k]);
+    stage_end(cir, cjr, tir, tjr);
     int32_t k1 = 0, k4 = 0;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
+    for (int k = 0; k < NP; ++k) {
         k1 += (uint64_t)jp[k] <= pk1 ? 1 : 0;
         k4 += (uint64_t)vp[k] <= pk4 ? 1 : 0;
     }
-    k1 = k1 < 7 ? k1 : 7;  // (8 only when s1 == 0, whose pick is redrawn below)
-    k4 = k4 < 7 ? k4 : 7;
+    k1 = k1 < NP - 1 ? k1 : NP - 1;  // (NP only when s1 == 0, whose pick is redrawn below)
+    k4 = k4 < NP - 1 ? k4 : NP - 1;
     const int32_t uc1 = clamp0(cir, B - 1);
     const int32_t uc2 = reloc ? rc2 : clamp0(cjr, B - 1);
     // stage 2: the two blocks; the uniform-mode cell loads and sizes
@@ -391,10 +394,11 @@ __device__ inline void start_add(uint16_t *start16, int32_t lo, int32_t hi, int3
     }
 }
 
-// Prefixes of the roulette weights into LDS (lane h holds J_h): J_pre and
-// V_h = (h + 1)(s2 + 1) - J_pre[h], with their pivot entries 8k+7; entries at
-// h >= RG hold kInf.
-__device__ inline void write_jpre(const Lds &M, int64_t Jr, int32_t RG, int64_t s2) {
+// Prefixes of the roulette weights into LDS (lane h holds J_h, and J_{h+64}
+// in Jr2 when RV == 2): J_pre and V_h = (h + 1)(s2 + 1) - J_pre[h], with
+// their pivot entries 8k+7; entries at h >= RG hold kInf.
+template <int RV>
+__device__ inline void write_jpre(const Lds &M, int64_t Jr, int64_t Jr2, int32_t RG, int64_t s2) {
     const int lane = lane_id();
     const int64_t incl = wave_incl_scan(lane < RG ? Jr : 0);
     const int64_t v = lane < RG ? incl : kInf;
@@ -405,6 +409,26 @@ __device__ inline void write_jpre(const Lds &M, int64_t Jr, int32_t RG, int64_t 
         M.Jpiv[lane >> 3] = v;
         M.Vpiv[lane >> 3] = t;
     }
+    if (RV == 2) {
+        const int32_t h = lane + kWave;
+        const int64_t incl2 = wave_incl_scan(h < RG ? Jr2 : 0) + (int64_t)readlane64((uint64_t)incl, kWave - 1);
+        const int64_t v2 = h < RG ? incl2 : kInf;
+        const int64_t t2 = h < RG ? (int64_t)(h + 1) * (s2 + 1) - incl2 : kInf;
+        M.Jpre[h] = v2;
+        M.Vpre[h] = t2;
+        if ((lane & 7) == 7) {
+            M.Jpiv[h >> 3] = v2;
+            M.Vpiv[h >> 3] = t2;
+        }
+    }
+}
+
+// A row-shard's entry of a lane-distributed table (row-shard h on lane h, or
+// on lane h - 64 of the second register when RV == 2); h is wave-uniform.
+template <int RV>
+__device__ inline int64_t row_entry(int64_t v, int64_t v2, int32_t h) {
+    if (RV == 1 || h < kWave) return (int64_t)readlane64((uint64_t)v, h);
+    return (int64_t)readlane64((uint64_t)v2, h - kWave);
 }
 
 // Member state kept in registers between proposals: J and A of the
@@ -412,6 +436,7 @@ __device__ inline void write_jpre(const Lds &M, int64_t Jr, int32_t RG, int64_t 
 // current score.
 struct Regs {
     int64_t Jr, Ar, Ur, s0, s1, s2;
+    int64_t Jr2, Ar2;  // row-shards 64..127 (more than 64 row-shards only)
 };
 
 // Member slab sections in HBM.
@@ -467,7 +492,7 @@ __device__ inline Tables load_tables(const AnnealArgs &a, char *smem) {
     for (int32_t x = threadIdx.x; x < n4; x += blockDim.x) reinterpret_cast<int4 *>(s_t)[x] = t4[x];
     for (int32_t x = (n4 << 2) + threadIdx.x; x < N; x += blockDim.x) s_t[x] = a.t[x];
     __syncthreads();
-    return Tables{s_slots, s_count, s_shard, s_soff, s_t, s_hcnt, s_hcell};    return Tables{s_slots, s_count, s_shard, s_soff, s_t};
+    return Tables{s_slots, s_count, s_shard, s_soff, s_t, s_hcnt, s_hcell};
 }
 
 __device__ inline Lds member_lds(const AnnealArgs &a, char *smem, int wv) {
@@ -481,15 +506,16 @@ __device__ inline Lds member_lds(const AnnealArgs &a, char *smem, int wv) {
     M.Cp = reinterpret_cast<int64_t *>(mine + a.o_acost);
     M.Ctot = M.Cp + a.RG * (a.dv + 1);
     M.Jpre = reinterpret_cast<int64_t *>(mine + a.o_Jpre);
-    M.Vpre = M.Jpre + 64;
-    M.Jpiv = M.Jpre + 128;
-    M.Vpiv = M.Jpre + 136;
+    M.Vpre = M.Jpre + 64 * a.rv;
+    M.Jpiv = M.Jpre + 128 * a.rv;
+    M.Vpiv = M.Jpiv + 8 * a.rv;
     return M;
 }
 
 // A member's state from a slab into LDS and registers (one wave).  The
 // global loads go out in batches of 16 per lane per array before any LDS
 // store, so a reload costs few memory round trips.
+template <int RV>
 __device__ inline void member_load(const AnnealArgs &a, const Lds &M, const Tables &tb, const SlabPtrs &g,
                                    Regs &R) {
     const int lane = lane_id();
@@ -545,17 +571,20 @@ __device__ inline void member_load(const AnnealArgs &a, const Lds &M, const Tabl
             }
         }
     }
+    const int32_t h2 = lane + kWave;  // the lane's second row-shard (more than 64 only)
     R.Jr = lane < RG ? g.J[lane] : 0;
     R.Ar = lane < RG ? g.A[lane] : 0;
+    R.Jr2 = RV == 2 && h2 < RG ? g.J[h2] : 0;
+    R.Ar2 = RV == 2 && h2 < RG ? g.A[h2] : 0;
     wsync();
     // cost prefix of each row-shard's cells, in slot order (lanes over row-shards)
-    if (lane < RG) {
-        const int32_t cnt = tb.hcnt[lane];
+    for (int32_t h = lane; h < (RV == 2 ? RG : (RG < kWave ? RG : kWave)); h += kWave) {
+        const int32_t cnt = tb.hcnt[h];
         int64_t acc = 0;
-        int64_t *cp = M.Cp + lane * (a.dv + 1);
+        int64_t *cp = M.Cp + h * (a.dv + 1);
         for (int32_t x = 0; x < a.dv; ++x) {
             if (x < cnt) {
-                const int32_t c = tb.hcell[lane * a.dv + x];
+                const int32_t c = tb.hcell[h * a.dv + x];
                 const int64_t t = M.T[c], q = M.Q[c];
                 for (int s = 0; s < a.S; ++s) acc += a.alpha[s] * t + a.beta[s] * q;
                 cp[x] = acc;
@@ -563,24 +592,26 @@ __device__ inline void member_load(const AnnealArgs &a, const Lds &M, const Tabl
                 cp[x] = kInf;
             }
         }
-        M.Ctot[lane] = acc;
+        M.Ctot[h] = acc;
     }
     // U_g = sum over rows of J(r, g); lane g holds it
     int64_t Ur = 0;
-    const int32_t gl = lane - (lane / G) * G;
+    const int32_t gl = lane - (lane / G) * G, gl2 = h2 - (h2 / G) * G;
     for (int32_t gg = 0; gg < G; ++gg) {
-        const int64_t u = wave_sum(lane < RG && gl == gg ? R.Jr : 0);
+        const int64_t u = wave_sum((lane < RG && gl == gg ? R.Jr : 0) + (RV == 2 && h2 < RG && gl2 == gg ? R.Jr2 : 0));
         if (lane == gg) Ur = u;
     }
     R.Ur = Ur;
     R.s0 = wave_max(lane < G ? Ur : LLONG_MIN);
     R.s1 = wave_sum(lane < G ? Ur : 0);
-    R.s2 = wave_max(lane < RG ? R.Jr : LLONG_MIN);
-    write_jpre(M, R.Jr, RG, R.s2);
+    const int64_t j1 = lane < RG ? R.Jr : LLONG_MIN, j2 = RV == 2 && h2 < RG ? R.Jr2 : LLONG_MIN;
+    R.s2 = wave_max(j1 > j2 ? j1 : j2);
+    write_jpre<RV>(M, R.Jr, R.Jr2, RG, R.s2);
     wsync();
 }
 
 // A member's state back to a slab (W is kept up to date in the slab).
+template <int RV>
 __device__ inline void member_store(const AnnealArgs &a, const Lds &M, const SlabPtrs &g, const Regs &R) {
     const int lane = lane_id();
     const int32_t N = a.N, B = a.B, RG = a.RG;
@@ -606,6 +637,10 @@ __device__ inline void member_store(const AnnealArgs &a, const Lds &M, const Sla
         g.J[lane] = R.Jr;
         g.A[lane] = R.Ar;
     }
+    if (RV == 2 && lane + kWave < RG) {
+        g.J[lane + kWave] = R.Jr2;
+        g.A[lane + kWave] = R.Ar2;
+    }
 }
 
 // One level (K proposals) of member m from its current state, at the given
@@ -617,14 +652,18 @@ struct LevelOut {
     double e;            // terminal energy
 };
 
+// GV selects the variant: 1 the common shape (see screen), 0 the general
+// one, 2 the general one with two row-shards per lane (65 to 128).
 template <int PV, int DV, int GV>
 __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const Tables &tb, int32_t *W, int m,
                                         int32_t level, double temp, int64_t x0, int64_t x1, int64_t x2,
                                         uint8_t *log_arg, int64_t *res, int64_t *trace_row, Regs &R) {
+    constexpr int RV = GV == 2 ? 2 : 1;
     uint8_t *const log = GV == 1 ? nullptr : log_arg;  // (the common shape is launched without a step log)
     const int lane = lane_id();
     const int32_t N = a.N, B = a.B, RG = a.RG, D = a.D, G = GV == 1 ? 1 : a.G, L = a.L;
     int64_t Jr = R.Jr, Ar = R.Ar, Ur = R.Ur, s0 = R.s0, s1 = R.s1, s2 = R.s2;
+    int64_t Jr2 = RV == 2 ? R.Jr2 : 0, Ar2 = RV == 2 ? R.Ar2 : 0;  // row-shards 64..127
     int64_t b0 = s0, b1 = s1, b2 = s2;
     int32_t best_is_start = 1;
     int32_t *bl = a.best + (int64_t)m * N;
@@ -667,7 +706,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
         const uint64_t w0 = b0w.v[0], w1 = b0w.v[1], w2 = b0w.v[2], w3 = b0w.v[3];
         const uint64_t w4 = b1w.v[0], w5 = b1w.v[1], w6 = b1w.v[2], w7 = b1w.v[3];
         uint64_t pending = __ballot(k < a.K);
-        Screen sc = screen<DV, GV>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
+        Screen sc = screen<DV, GV, RV>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
         uint64_t feas = __ballot(sc.feas && k < a.K);
         uint64_t valid = ~0ull;  // lanes whose screen is current
         while (pending) {
@@ -677,7 +716,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                 // current; otherwise screen the batch again.
                 const uint64_t stale = pending & ~valid;
                 if (stale && (!cand || (stale & (~stale + 1)) <= (cand & (~cand + 1)))) {
-                    sc = screen<DV, GV>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
+                    sc = screen<DV, GV, RV>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
                     feas = __ballot(sc.feas && k < a.K);
                     valid = ~0ull;
                     cand = pending & feas;
@@ -764,8 +803,8 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
             }
             const int64_t Aa = (int64_t)readlane64((uint64_t)Arow, 0);
             const int64_t Ab = two ? (int64_t)readlane64((uint64_t)Arow, 32) : Aa;
-            const int64_t Jha = (int64_t)readlane64((uint64_t)Jr, ha), Aha = (int64_t)readlane64((uint64_t)Ar, ha);
-            const int64_t Jhb = (int64_t)readlane64((uint64_t)Jr, hb);
+            const int64_t Jha = row_entry<RV>(Jr, Jr2, ha), Aha = row_entry<RV>(Ar, Ar2, ha);
+            const int64_t Jhb = row_entry<RV>(Jr, Jr2, hb);
             int64_t Ja, Jb;
             int32_t nw[PV];
             if (two) {
@@ -819,14 +858,20 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                     n0 = wave_max(lane < G ? Un : LLONG_MIN);
                 }
             }
-            const int64_t Jn = lane == ha ? Ja : (lane == hb ? Jb : Jr);
             // the maximum of the other row-shards is s2 unless ha or hb held it
             int64_t n2;
             if (Jha < s2 && Jhb < s2) {
                 n2 = s2 > Ja ? s2 : Ja;
                 n2 = n2 > Jb ? n2 : Jb;
             } else {
-                n2 = wave_max(lane < RG ? Jn : LLONG_MIN);
+                const int64_t Jn = lane == ha ? Ja : (lane == hb ? Jb : Jr);
+                int64_t mx = lane < RG ? Jn : LLONG_MIN;
+                if (RV == 2) {
+                    const int32_t h2 = lane + kWave;
+                    const int64_t Jn2 = h2 == ha ? Ja : (h2 == hb ? Jb : Jr2);
+                    mx = h2 < RG && Jn2 > mx ? Jn2 : mx;
+                }
+                n2 = wave_max(mx);
             }
             const double e_new = GV == 1 ? energy_pow2(a, n0, n1, n2) : energy_k(a, n0, n1, n2);
             bool accept = lex_less(n0, n1, n2, s0, s1, s2);
@@ -921,7 +966,16 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                 Jr = Jb;
                 Ar = Ab;
             }
-            write_jpre(M, Jr, RG, n2);
+            if (RV == 2) {
+                if (lane + kWave == ha) {
+                    Jr2 = Ja;
+                    Ar2 = Aa;
+                } else if (lane + kWave == hb) {
+                    Jr2 = Jb;
+                    Ar2 = Ab;
+                }
+            }
+            write_jpre<RV>(M, Jr, Jr2, RG, n2);
             if (pending) {
                 // A screen stays current unless the move touched what it
                 // read: its cells (lengths, members, sizes), the cell costs
@@ -969,6 +1023,10 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
     }
     R.Jr = Jr;
     R.Ar = Ar;
+    if (RV == 2) {
+        R.Jr2 = Jr2;
+        R.Ar2 = Ar2;
+    }
     R.Ur = Ur;
     R.s0 = s0;
     R.s1 = s1;
@@ -1002,11 +1060,11 @@ __global__ void __launch_bounds__(512) k_anneal_chain(AnnealArgs a) {
     const Lds M = member_lds(a, smem, wv);
     const SlabPtrs g = slab_ptrs(a, a.slabs + (int64_t)a.slab_of[m] * a.off.bytes);
     Regs R;
-    member_load(a, M, tb, g, R);
+    member_load<GV == 2 ? 2 : 1>(a, M, tb, g, R);
     member_level<PV, DV, GV>(a, M, tb, g.W, m, a.level, a.temp, a.xscore[0], a.xscore[1], a.xscore[2],
                          a.step_log ? a.step_log + (int64_t)m * a.K : nullptr, a.results + (int64_t)m * kRes,
                          nullptr, R);
-    member_store(a, M, g, R);
+    member_store<GV == 2 ? 2 : 1>(a, M, g, R);
 }
 
 // ---------------------------------------------------------------------------
@@ -1029,6 +1087,7 @@ constexpr unsigned kSpinLimit = 1u << 22;
 // region (16-byte units, all reads then all writes per batch) and the
 // registers.  Every lane of the wave takes part.
 typedef int32_t v4i __attribute__((ext_vector_type(4)));
+template <int RV>
 __device__ inline void member_publish(const AnnealArgs &a, const char *mine, char *blob, const Regs &R) {
     const int lane = lane_id();
     wsync();
@@ -1053,12 +1112,17 @@ __device__ inline void member_publish(const AnnealArgs &a, const char *mine, cha
     rg[lane] = R.Jr;
     rg[kWave + lane] = R.Ar;
     rg[2 * kWave + lane] = R.Ur;
+    if (RV == 2) {
+        rg[3 * kWave + 3 + lane] = R.Jr2;
+        rg[4 * kWave + 3 + lane] = R.Ar2;
+    }
     if (lane == 0) {
         rg[3 * kWave] = R.s0;
         rg[3 * kWave + 1] = R.s1;
         rg[3 * kWave + 2] = R.s2;
     }
 }
+template <int RV>
 __device__ inline void member_receive(const AnnealArgs &a, char *mine, const char *blob, Regs &R) {
     const int lane = lane_id();
     const int32_t n16 = a.lds_member >> 4;
@@ -1068,6 +1132,10 @@ __device__ inline void member_receive(const AnnealArgs &a, char *mine, const cha
     R.Jr = rg[lane];
     R.Ar = rg[kWave + lane];
     R.Ur = rg[2 * kWave + lane];
+    if (RV == 2) {
+        R.Jr2 = rg[3 * kWave + 3 + lane];
+        R.Ar2 = rg[4 * kWave + 3 + lane];
+    }
     R.s0 = rg[3 * kWave];
     R.s1 = rg[3 * kWave + 1];
     R.s2 = rg[3 * kWave + 2];
@@ -1227,7 +1295,7 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
     if (active) {
         M = member_lds(a, smem, wv);
         g = slab_ptrs(a, a.slabs + (int64_t)gw * a.off.bytes);
-        member_load(a, M, tb, g, R);
+        member_load<GV == 2 ? 2 : 1>(a, M, tb, g, R);
     }
     unsigned epoch = 0;
     const uint64_t P = (uint64_t)pop;
@@ -1398,7 +1466,7 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
             // Every further child gets its parent's W in its own slab; the
             // copies are split evenly over all workgroups.
             {
-                // units <= pop * nW16 < 2^31: nW16 <= 64 * 32 * 16 / 4 and the
+                // units <= pop * nW16 < 2^31: nW16 <= 128 * 32 * 16 / 4 and the
                 // level-end tables in LDS hold pop below 6000
                 const int32_t *dups = reinterpret_cast<const int32_t *>(Fs);
                 const int32_t units = (int32_t)tdup * nW16;
@@ -1425,18 +1493,18 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
                 }
             }
             // and the rest of its state from the parent's own slab
-            if (publish) member_publish(a, smem + a.lds_shared + (int64_t)wv * a.lds_member, r.blobs + (int64_t)gw * r.blob_bytes, R);
+            if (publish) member_publish<GV == 2 ? 2 : 1>(a, smem + a.lds_shared + (int64_t)wv * a.lds_member, r.blobs + (int64_t)gw * r.blob_bytes, R);
         }
         if (!grid_sync(r.bar, (unsigned)nb * ++epoch, r.err, &s_ok)) return;  // B
         if (resample) {
             if (active && src_slab >= 0)
-                member_receive(a, smem + a.lds_shared + (int64_t)wv * a.lds_member, r.blobs + (int64_t)src_slab * r.blob_bytes, R);
+                member_receive<GV == 2 ? 2 : 1>(a, smem + a.lds_shared + (int64_t)wv * a.lds_member, r.blobs + (int64_t)src_slab * r.blob_bytes, R);
             for (int32_t mm = tid; mm < pop; mm += nt) slab[mm] = slabn[mm];
             __syncthreads();
         }
         m = m_next;
     }
-    if (active) member_store(a, M, g, R);
+    if (active) member_store<GV == 2 ? 2 : 1>(a, M, g, R);
     if (blockIdx.x == 0)
         for (int32_t mm = tid; mm < pop; mm += nt) r.slab_of_out[mm] = slab[mm];
 }
@@ -1479,8 +1547,9 @@ int chain_prepare(AnnealArgs &a, int32_t *qt, hipStream_t stream) {
 bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out, int32_t *dv_out) {
     const int32_t P = a.P;
     if (!(P == 4 || P == 8 || P == 16)) return false;
-    if (a.L > 32 || a.RG > kWave || max_count > 16 || a.N > 65535 || a.B + 1 > 65535 || a.C > 2147483647LL)
+    if (a.L > 32 || a.RG > 2 * kWave || max_count > 16 || a.N > 65535 || a.B + 1 > 65535 || a.C > 2147483647LL)
         return false;
+    a.rv = a.RG > kWave ? 2 : 1;  // row-shards per lane
     const int32_t dv = max_count <= 8 ? 8 : 16;
     auto up16 = [](int64_t x) { return (x + 15) & ~(int64_t)15; };
     auto up8e = [](int64_t n) { return ((n + 7) & ~(int64_t)7) + 16; };  // elements, padded for 16-byte steps
@@ -1492,8 +1561,8 @@ bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out,
     a.o_Q = (int32_t)o; o = up16(o + 8 * (int64_t)a.B);
     a.dv = dv;
     a.o_acost = (int32_t)o; o = up16(o + 8 * ((int64_t)a.RG * (dv + 1) + a.RG));  // cost prefixes and totals
-    a.o_Jpre = (int32_t)o; o = up16(o + 8 * (64 + 64 + 8 + 8));  // J_pre, V_pre and their pivots
-    a.o_Jpiv = a.o_Jpre + 8 * 128;
+    a.o_Jpre = (int32_t)o; o = up16(o + 8 * 144 * (int64_t)a.rv);  // J_pre, V_pre and their pivots
+    a.o_Jpiv = a.o_Jpre + 8 * 128 * a.rv;
     a.ginv = (uint32_t)((((uint64_t)1 << 32) + (uint64_t)a.G - 1) / (uint64_t)a.G);
     a.dinv = (uint32_t)((((uint64_t)1 << 32) + (uint64_t)a.D - 1) / (uint64_t)a.D);
     a.dshift = -1;
@@ -1557,40 +1626,61 @@ static int chain_run_t(const AnnealArgs &a, const RunArgs &r0, int32_t n_cu, boo
     return hipGetLastError() == hipSuccess ? ROUTEPACK_OK : ROUTEPACK_E_DEVICE;
 }
 
+// The variant of the chain kernels for this problem: 2 with more than 64
+// row-shards, else 1 for the common shape and 0 for the general one.
+static int chain_variant(const AnnealArgs &a, bool step_log) {
+    if (a.rv == 2) return 2;
+    return a.G == 1 && a.dshift >= 0 && a.S == 1 && a.sum32 && a.scale_pow2 && !step_log ? 1 : 0;
+}
+
+template <int PV, int DV>
+static int chain_run_v(int v, const AnnealArgs &a, const RunArgs &r, int32_t n_cu, bool launch, hipStream_t stream) {
+    if (v == 2) return chain_run_t<PV, DV, 2>(a, r, n_cu, launch, stream);
+    if (v == 1) return chain_run_t<PV, DV, 1>(a, r, n_cu, launch, stream);
+    return chain_run_t<PV, DV, 0>(a, r, n_cu, launch, stream);
+}
+
 // Checks (launch = false) or launches (launch = true) the whole-schedule
 // kernel; ROUTEPACK_E_UNSUPPORTED when its workgroups cannot all be resident.
 int chain_run(const AnnealArgs &a, const RunArgs &r, int32_t pv, int32_t dv, int32_t n_cu, bool launch,
               hipStream_t stream) {
-    const bool g1 = a.G == 1 && a.dshift >= 0 && a.S == 1 && a.sum32 && a.scale_pow2 && !r.step_log;  // the common shape
+    const int v = chain_variant(a, r.step_log != nullptr);
     if (dv == 8) {
         switch (pv) {
-            case 4: return g1 ? chain_run_t<4, 8, 1>(a, r, n_cu, launch, stream) : chain_run_t<4, 8, 0>(a, r, n_cu, launch, stream);
-            case 8: return g1 ? chain_run_t<8, 8, 1>(a, r, n_cu, launch, stream) : chain_run_t<8, 8, 0>(a, r, n_cu, launch, stream);
-            case 16: return g1 ? chain_run_t<16, 8, 1>(a, r, n_cu, launch, stream) : chain_run_t<16, 8, 0>(a, r, n_cu, launch, stream);
+            case 4: return chain_run_v<4, 8>(v, a, r, n_cu, launch, stream);
+            case 8: return chain_run_v<8, 8>(v, a, r, n_cu, launch, stream);
+            case 16: return chain_run_v<16, 8>(v, a, r, n_cu, launch, stream);
         }
     } else {
         switch (pv) {
-            case 4: return g1 ? chain_run_t<4, 16, 1>(a, r, n_cu, launch, stream) : chain_run_t<4, 16, 0>(a, r, n_cu, launch, stream);
-            case 8: return g1 ? chain_run_t<8, 16, 1>(a, r, n_cu, launch, stream) : chain_run_t<8, 16, 0>(a, r, n_cu, launch, stream);
-            case 16: return g1 ? chain_run_t<16, 16, 1>(a, r, n_cu, launch, stream) : chain_run_t<16, 16, 0>(a, r, n_cu, launch, stream);
+            case 4: return chain_run_v<4, 16>(v, a, r, n_cu, launch, stream);
+            case 8: return chain_run_v<8, 16>(v, a, r, n_cu, launch, stream);
+            case 16: return chain_run_v<16, 16>(v, a, r, n_cu, launch, stream);
         }
     }
     return ROUTEPACK_E_UNSUPPORTED;
 }
 
+template <int PV, int DV>
+static int chain_launch_v(int v, const AnnealArgs &a, hipStream_t stream) {
+    if (v == 2) return chain_launch_t<PV, DV, 2>(a, stream);
+    if (v == 1) return chain_launch_t<PV, DV, 1>(a, stream);
+    return chain_launch_t<PV, DV, 0>(a, stream);
+}
+
 int launch_anneal_chain(const AnnealArgs &a, int32_t pv, int32_t dv, hipStream_t stream) {
-    const bool g1 = a.G == 1 && a.dshift >= 0 && a.S == 1 && a.sum32 && a.scale_pow2 && !a.step_log;  // the common shape
+    const int v = chain_variant(a, a.step_log != nullptr);
     if (dv == 8) {
         switch (pv) {
-            case 4: return g1 ? chain_launch_t<4, 8, 1>(a, stream) : chain_launch_t<4, 8, 0>(a, stream);
-            case 8: return g1 ? chain_launch_t<8, 8, 1>(a, stream) : chain_launch_t<8, 8, 0>(a, stream);
-            case 16: return g1 ? chain_launch_t<16, 8, 1>(a, stream) : chain_launch_t<16, 8, 0>(a, stream);
+            case 4: return chain_launch_v<4, 8>(v, a, stream);
+            case 8: return chain_launch_v<8, 8>(v, a, stream);
+            case 16: return chain_launch_v<16, 8>(v, a, stream);
         }
     } else {
         switch (pv) {
-            case 4: return g1 ? chain_launch_t<4, 16, 1>(a, stream) : chain_launch_t<4, 16, 0>(a, stream);
-            case 8: return g1 ? chain_launch_t<8, 16, 1>(a, stream) : chain_launch_t<8, 16, 0>(a, stream);
-            case 16: return g1 ? chain_launch_t<16, 16, 1>(a, stream) : chain_launch_t<16, 16, 0>(a, stream);
+            case 4: return chain_launch_v<4, 16>(v, a, stream);
+            case 8: return chain_launch_v<8, 16>(v, a, stream);
+            case 16: return chain_launch_v<16, 16>(v, a, stream);
         }
     }
     return ROUTEPACK_E_UNSUPPORTED;
