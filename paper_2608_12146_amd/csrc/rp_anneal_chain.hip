@@ -35,12 +35,26 @@ __device__ inline void wsync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Inclusive prefix sum within each 16-lane row.
+// Inclusive prefix sum over the first W lanes (W = 8 or 16) of each 16-lane
+// row.
+template <int W>
 __device__ inline int64_t row_incl_scan64(int64_t v) {
     v += dpp64<kDppRowShr1>(v, 0);
     v += dpp64<kDppRowShr1 + 1>(v, 0);
     v += dpp64<kDppRowShr1 + 3>(v, 0);
-    v += dpp64<kDppRowShr1 + 7>(v, 0);
+    if (W > 8) v += dpp64<kDppRowShr1 + 7>(v, 0);
+    return v;
+}
+
+// Maximum over the first W lanes (W = 8 or 16) of each 16-lane row, held by
+// those lanes.
+template <int W>
+__device__ inline int64_t row_head_max64(int64_t v) {
+    if (W > 8) return row_max64(v);
+    int64_t o;
+    o = dpp64<kDppXor1>(v, v); v = o > v ? o : v;
+    o = dpp64<kDppXor2>(v, v); v = o > v ? o : v;
+    o = dpp64<kDppHalfMirror>(v, v); v = o > v ? o : v;
     return v;
 }
 
@@ -394,13 +408,13 @@ __device__ inline void start_add(uint16_t *start16, int32_t lo, int32_t hi, int3
     }
 }
 
-// Prefixes of the roulette weights into LDS (lane h holds J_h, and J_{h+64}
-// in Jr2 when RV == 2): J_pre and V_h = (h + 1)(s2 + 1) - J_pre[h], with
-// their pivot entries 8k+7; entries at h >= RG hold kInf.
+// Prefixes of the roulette weights into LDS from J_pre (lane h holds
+// J_pre[h], and J_pre[h + 64] in Jp2 when RV == 2): J_pre and
+// V_h = (h + 1)(s2 + 1) - J_pre[h], with their pivot entries 8k+7; entries at
+// h >= RG hold kInf.
 template <int RV>
-__device__ inline void write_jpre(const Lds &M, int64_t Jr, int64_t Jr2, int32_t RG, int64_t s2) {
+__device__ inline void write_prefix(const Lds &M, int64_t incl, int64_t incl2, int32_t RG, int64_t s2) {
     const int lane = lane_id();
-    const int64_t incl = wave_incl_scan(lane < RG ? Jr : 0);
     const int64_t v = lane < RG ? incl : kInf;
     const int64_t t = lane < RG ? (int64_t)(lane + 1) * (s2 + 1) - incl : kInf;
     M.Jpre[lane] = v;
@@ -411,7 +425,6 @@ __device__ inline void write_jpre(const Lds &M, int64_t Jr, int64_t Jr2, int32_t
     }
     if (RV == 2) {
         const int32_t h = lane + kWave;
-        const int64_t incl2 = wave_incl_scan(h < RG ? Jr2 : 0) + (int64_t)readlane64((uint64_t)incl, kWave - 1);
         const int64_t v2 = h < RG ? incl2 : kInf;
         const int64_t t2 = h < RG ? (int64_t)(h + 1) * (s2 + 1) - incl2 : kInf;
         M.Jpre[h] = v2;
@@ -421,6 +434,23 @@ __device__ inline void write_jpre(const Lds &M, int64_t Jr, int64_t Jr2, int32_t
             M.Vpiv[h >> 3] = t2;
         }
     }
+}
+
+// J_pre of the lane's row-shards (h = lane, and lane + 64 in the second
+// value when RV == 2) from their J values.
+template <int RV>
+__device__ inline void j_prefix(int64_t Jr, int64_t Jr2, int32_t RG, int64_t &incl, int64_t &incl2) {
+    const int lane = lane_id();
+    incl = wave_incl_scan(lane < RG ? Jr : 0);
+    incl2 = RV == 2 ? wave_incl_scan(lane + kWave < RG ? Jr2 : 0) + (int64_t)readlane64((uint64_t)incl, kWave - 1)
+                    : 0;
+}
+
+template <int RV>
+__device__ inline void write_jpre(const Lds &M, int64_t Jr, int64_t Jr2, int32_t RG, int64_t s2) {
+    int64_t incl, incl2;
+    j_prefix<RV>(Jr, Jr2, RG, incl, incl2);
+    write_prefix<RV>(M, incl, incl2, RG, s2);
 }
 
 // A row-shard's entry of a lane-distributed table (row-shard h on lane h, or
@@ -664,6 +694,9 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
     const int32_t N = a.N, B = a.B, RG = a.RG, D = a.D, G = GV == 1 ? 1 : a.G, L = a.L;
     int64_t Jr = R.Jr, Ar = R.Ar, Ur = R.Ur, s0 = R.s0, s1 = R.s1, s2 = R.s2;
     int64_t Jr2 = RV == 2 ? R.Jr2 : 0, Ar2 = RV == 2 ? R.Ar2 : 0;  // row-shards 64..127
+    // J_pre of the lane's row-shards, kept up to date by each move's J deltas
+    int64_t Jp, Jp2;
+    j_prefix<RV>(Jr, Jr2, RG, Jp, Jp2);
     int64_t b0 = s0, b1 = s1, b2 = s2;
     int32_t best_is_start = 1;
     int32_t *bl = a.best + (int64_t)m * N;
@@ -798,7 +831,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                 if (s < (GV == 1 ? 1 : a.S)) {
                     const int64_t cost = a.alpha[s] * Tc + a.beta[s] * Qc;
                     cw += cact ? cost : 0;
-                    Arow = (int64_t)((uint64_t)Arow + (uint64_t)row_max64(cact ? cost : LLONG_MIN));
+                    Arow = (int64_t)((uint64_t)Arow + (uint64_t)row_head_max64<DV>(cact ? cost : LLONG_MIN));
                 }
             }
             const int64_t Aa = (int64_t)readlane64((uint64_t)Arow, 0);
@@ -955,7 +988,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                 M.Q[c2] = nQ2;
             }
             {
-                const int64_t incl = row_incl_scan64(cw);
+                const int64_t incl = row_incl_scan64<DV>(cw);
                 if (cact) M.Cp[hsel * (DV + 1) + cx] = incl;
                 if (cact && cx == cnt - 1) M.Ctot[hsel] = incl;
             }
@@ -975,7 +1008,11 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                     Ar2 = Ab;
                 }
             }
-            write_jpre<RV>(M, Jr, Jr2, RG, n2);
+            // J_pre moves by dJa from row-shard ha on and by dJb from hb on
+            auto shift = [&](int32_t h) -> int64_t { return (h >= ha ? dJa : 0) + (h >= hb ? dJb : 0); };
+            Jp += shift(lane);
+            if (RV == 2) Jp2 += shift(lane + kWave);
+            write_prefix<RV>(M, Jp, Jp2, RG, n2);
             if (pending) {
                 // A screen stays current unless the move touched what it
                 // read: its cells (lengths, members, sizes), the cell costs
@@ -984,7 +1021,6 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                 // in the interval after the move's J deltas; V_pre moves by
                 // (h + 1)(n2 - s2) besides.  A relocation shifts the members
                 // of the cells strictly between its two cells by one place.
-                auto shift = [&](int32_t h) -> int64_t { return (h >= ha ? dJa : 0) + (h >= hb ? dJb : 0); };
                 const int64_t ds2 = n2 - s2;
                 sc.jlo += shift(sc.h1 - 1);
                 sc.jhi += shift(sc.h1);
