@@ -75,12 +75,14 @@ struct RunArgs {
     unsigned *bar;         // grid barrier arrivals (zero at launch)
     int32_t *err;          // set when a grid barrier times out
     int32_t *slab_of_out;  // [pop] slab of each member after the run
-    double *energy;        // [pop] terminal energy of each member (per level)
-    int64_t *wg_best;      // [workgroups][4] lexicographic-min trajectory best and its member
-    double *wg_emin;       // [workgroups] minimum terminal energy
+    double *energy;        // [2][pop] terminal energy of each member (by level parity)
+    int64_t *wg_best;      // [2][workgroups][4] lexicographic-min trajectory best and its member
+    double *wg_emin;       // [2][workgroups] minimum terminal energy
     int32_t o_lend;        // LDS offset of the level-end tables
     char *blobs;           // [pop][blob_bytes]: a published member's LDS image and registers, per slab
     int64_t blob_bytes;
+    unsigned *pub;         // [pop] per slab: the last level whose image it published (zero at launch)
+    unsigned *got;         // [pop] per slab: receivers that have copied its image (zero at launch)
 };
 
 // Bytes of one hand-over image: the member's LDS region, then J, A and U of

@@ -1175,15 +1175,19 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
         double *temps_d = scr.get<double>(prm->n_sweeps);
         unsigned *bar = scr.get<unsigned>(2);
         int32_t *slab_final = scr.get<int32_t>(pop_size);
-        double *energy_d = scr.get<double>(pop_size);
-        int64_t *wg_best = scr.get<int64_t>((size_t)4 * pop_size);
-        double *wg_emin = scr.get<double>(pop_size);
+        // by level parity: a workgroup that runs ahead into the next level
+        // writes the other half
+        double *energy_d = scr.get<double>((size_t)2 * pop_size);
+        int64_t *wg_best = scr.get<int64_t>((size_t)8 * pop_size);
+        double *wg_emin = scr.get<double>((size_t)2 * pop_size);
+        unsigned *flags = scr.get<unsigned>((size_t)2 * pop_size);  // hand-over flags and counts
         const int64_t blob_bytes = run_blob_bytes(a.lds_member);
         char *blobs = scr.get<char>((size_t)pop_size * (size_t)blob_bytes);
         if (scr.failed()) return ROUTEPACK_E_DEVICE;
         RP_HIP(hipMemcpyAsync(temps_d, prm->temperatures, sizeof(double) * prm->n_sweeps, hipMemcpyHostToDevice,
                               stream));
         RP_HIP(hipMemsetAsync(bar, 0, 2 * sizeof(unsigned), stream));
+        RP_HIP(hipMemsetAsync(flags, 0, 2 * sizeof(unsigned) * (size_t)pop_size, stream));
         a.slabs = slabA;
         a.xscore = best_score;
         run.temps = temps_d;
@@ -1203,6 +1207,8 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
         run.wg_emin = wg_emin;
         run.blobs = blobs;
         run.blob_bytes = blob_bytes;
+        run.pub = flags;
+        run.got = flags + pop_size;
         hipEvent_t e0 = nullptr, e1 = nullptr;
         if (prm->level_kernel_ms) {
             RP_HIP(hipEventCreate(&e0));

@@ -1123,6 +1123,28 @@ constexpr unsigned kSpinLimit = 1u << 22;
 // region (16-byte units, all reads then all writes per batch) and the
 // registers.  Every lane of the wave takes part.
 typedef int32_t v4i __attribute__((ext_vector_type(4)));
+// Copies n 16-byte units from src to dst with one wave, 16 loads per lane in
+// flight before the stores.
+__device__ inline void wave_copy16(const char *src, char *dst, int32_t n) {
+    const v4i *s4 = reinterpret_cast<const v4i *>(src);
+    v4i *d4 = reinterpret_cast<v4i *>(dst);
+    const int lane = lane_id();
+    constexpr int U = 16;
+    for (int32_t base = 0; base < n; base += U * kWave) {
+        v4i v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int32_t x = base + u * kWave + lane;
+            v[u] = s4[x < n ? x : n - 1];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int32_t x = base + u * kWave + lane;
+            if (x < n) d4[x] = v[u];
+        }
+    }
+}
+
 template <int RV>
 __device__ inline void member_publish(const AnnealArgs &a, const char *mine, char *blob, const Regs &R) {
     const int lane = lane_id();
@@ -1216,6 +1238,28 @@ __device__ inline bool grid_sync(unsigned *bar, unsigned target, int32_t *err, i
     }
     __syncthreads();
     return *s_ok != 0;
+}
+
+// Waits (one wave) until *p >= target, then acquires; false if it timed
+// out or another wait or barrier failed (the error flag is set).
+__device__ inline bool wave_wait_geq(const unsigned *p, unsigned target, int32_t *err) {
+    unsigned spins = 0;
+    for (;;) {
+        unsigned v = 0;
+        if (lane_id() == 0) v = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if ((unsigned)__builtin_amdgcn_readlane((int)v, 0) >= target) break;
+        __builtin_amdgcn_s_sleep(2);
+        if ((++spins & 31) == 0) {
+            int32_t e = 0;
+            if (lane_id() == 0) e = __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (spins > kSpinLimit || __builtin_amdgcn_readlane(e, 0)) {
+                if (lane_id() == 0) __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                return false;
+            }
+        }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    return true;
 }
 
 // Systematic-resampling parent of a child: the first j with
@@ -1347,7 +1391,7 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
                 a, M, tb, g.W, m, level, temp, s_xs[0], s_xs[1], s_xs[2],
                 r.step_log ? r.step_log + ((int64_t)n * pop + m) * K : nullptr, a.results + (int64_t)m * kRes,
                 r.trace ? r.trace + ((int64_t)n * pop + m) * 8 : nullptr, R);
-            if (lane == 0) r.energy[m] = lo.e;
+            if (lane == 0) r.energy[(int64_t)(n & 1) * pop + m] = lo.e;
             k0 = lo.b0;
             k1 = lo.b1;
             k2 = lo.b2;
@@ -1367,8 +1411,8 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
                     for (int f = 0; f < 4; ++f) s_k[0][f] = s_k[w][f];
                 s_dred[0] = s_dred[w] < s_dred[0] ? s_dred[w] : s_dred[0];
             }
-            for (int f = 0; f < 4; ++f) r.wg_best[(int64_t)blockIdx.x * 4 + f] = s_k[0][f];
-            r.wg_emin[blockIdx.x] = s_dred[0];
+            for (int f = 0; f < 4; ++f) r.wg_best[((int64_t)(n & 1) * nb + blockIdx.x) * 4 + f] = s_k[0][f];
+            r.wg_emin[(n & 1) * nb + blockIdx.x] = s_dred[0];
         }
         if (!grid_sync(r.bar, (unsigned)nb * ++epoch, r.err, &s_ok)) return;  // A
 
@@ -1381,9 +1425,9 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
             k0 = k1 = k2 = kj = LLONG_MAX;
             emin = __builtin_inf();
             for (int b = tid; b < nb; b += nt) {
-                const int64_t *wb = r.wg_best + (int64_t)b * 4;
+                const int64_t *wb = r.wg_best + ((int64_t)(n & 1) * nb + b) * 4;
                 const int64_t v0 = wb[0], v1 = wb[1], v2 = wb[2], vj = wb[3];
-                const double e = r.wg_emin[b];
+                const double e = r.wg_emin[(n & 1) * nb + b];
                 if (lex_less(v0, v1, v2, k0, k1, k2) || (v0 == k0 && v1 == k1 && v2 == k2 && vj < kj)) {
                     k0 = v0; k1 = v1; k2 = v2; kj = vj;
                 }
@@ -1396,7 +1440,7 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
                 s_dred[wv] = emin;
             }
             // the energies of this thread's members (used by the resampling weights)
-            for (int32_t j = jlo; j < jhi; ++j) Fs[j] = __builtin_bit_cast(uint64_t, r.energy[j]);
+            for (int32_t j = jlo; j < jhi; ++j) Fs[j] = __builtin_bit_cast(uint64_t, r.energy[(int64_t)(n & 1) * pop + j]);
             __syncthreads();
             if (tid == 0) {
                 for (int w = 1; w < nwv; ++w) {
@@ -1462,14 +1506,26 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
                 r.parents_out[(int64_t)n * pop + mm] = resample ? par[mm] : -1;
         }
         // ---- slab hand-over
-        int32_t m_next = m, src_slab = -1;
+        // A level that moved the incumbent ends with grid barrier B (x* is
+        // copied from a member's trajectory-best row, which the next level
+        // may overwrite).  Otherwise the hand-over is point to point: a
+        // publisher releases its image with a flag; each receiver waits for
+        // that flag, copies the image and the parent's W into its own slab
+        // and counts itself in; the publisher, whose first child keeps the
+        // parent's slab, waits for that count before its next level changes
+        // W.  s_win is the same in every workgroup, so all of them take the
+        // same path.
+        const bool sync_b = s_win >= 0;
+        const unsigned token = (unsigned)n + 1;  // (flags are zero at launch)
+        int32_t m_next = m, src_slab = -1, n_recv = 0;
+        bool publish = false;
         if (resample) {
             // bit 0: the member has a child; bit 1: a second one
             for (int32_t mm = tid; mm < pop; mm += nt)
                 atomicOr(&flag[par[mm]], (mm > 0 && par[mm - 1] == par[mm]) ? 3 : 1);
             __syncthreads();
             // the current member publishes its state when it has a second child
-            const bool publish = active && (flag[m] & 2) != 0;
+            publish = active && (flag[m] & 2) != 0;
             int32_t n_dead = 0, n_dup = 0;
             for (int32_t j = jlo; j < jhi; ++j) {
                 n_dead += (flag[j] & 1) == 0;
@@ -1498,10 +1554,15 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
                 m_next = flag[gw];
                 const int32_t pn = par[m_next];
                 if (m_next > 0 && par[m_next - 1] == pn) src_slab = slab[pn];
+                if (publish) {  // the further children of this member
+                    int32_t c = m_next + 1;
+                    while (c < pop && par[c] == pn) ++c;
+                    n_recv = c - m_next - 1;
+                }
             }
-            // Every further child gets its parent's W in its own slab; the
-            // copies are split evenly over all workgroups.
-            {
+            // Every further child gets its parent's W in its own slab; with
+            // barrier B the copies are split evenly over all workgroups.
+            if (sync_b) {
                 // units <= pop * nW16 < 2^31: nW16 <= 128 * 32 * 16 / 4 and the
                 // level-end tables in LDS hold pop below 6000
                 const int32_t *dups = reinterpret_cast<const int32_t *>(Fs);
@@ -1529,14 +1590,30 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
                 }
             }
             // and the rest of its state from the parent's own slab
-            if (publish) member_publish<GV == 2 ? 2 : 1>(a, smem + a.lds_shared + (int64_t)wv * a.lds_member, r.blobs + (int64_t)gw * r.blob_bytes, R);
+            if (publish) {
+                member_publish<GV == 2 ? 2 : 1>(a, smem + a.lds_shared + (int64_t)wv * a.lds_member, r.blobs + (int64_t)gw * r.blob_bytes, R);
+                if (!sync_b) {
+                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+                    if (lane == 0) __hip_atomic_store(r.pub + gw, token, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
         }
-        if (!grid_sync(r.bar, (unsigned)nb * ++epoch, r.err, &s_ok)) return;  // B
+        if (sync_b && !grid_sync(r.bar, (unsigned)nb * ++epoch, r.err, &s_ok)) return;  // B
         if (resample) {
-            if (active && src_slab >= 0)
-                member_receive<GV == 2 ? 2 : 1>(a, smem + a.lds_shared + (int64_t)wv * a.lds_member, r.blobs + (int64_t)src_slab * r.blob_bytes, R);
             for (int32_t mm = tid; mm < pop; mm += nt) slab[mm] = slabn[mm];
             __syncthreads();
+            char *mine = smem + a.lds_shared + (int64_t)wv * a.lds_member;
+            if (active && src_slab >= 0 && (sync_b || wave_wait_geq(r.pub + src_slab, token, r.err))) {
+                member_receive<GV == 2 ? 2 : 1>(a, mine, r.blobs + (int64_t)src_slab * r.blob_bytes, R);
+                if (!sync_b) {
+                    wave_copy16(a.slabs + (int64_t)src_slab * a.off.bytes + a.off.W,
+                                a.slabs + (int64_t)gw * a.off.bytes + a.off.W, nW16);
+                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+                    if (lane == 0) __hip_atomic_fetch_add(r.got + src_slab, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
+            if (!sync_b && publish && wave_wait_geq(r.got + gw, (unsigned)n_recv, r.err) && lane == 0)
+                __hip_atomic_store(r.got + gw, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         m = m_next;
     }
