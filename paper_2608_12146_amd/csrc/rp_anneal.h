@@ -79,11 +79,16 @@ struct RunArgs {
     int64_t *wg_best;      // [2][workgroups][4] lexicographic-min trajectory best and its member
     double *wg_emin;       // [2][workgroups] minimum terminal energy
     int32_t o_lend;        // LDS offset of the level-end tables
+    char *lend;            // [workgroups][lend_stride] level-end tables in HBM (two row-shards per lane)
+    int64_t lend_stride;
     char *blobs;           // [pop][blob_bytes]: a published member's LDS image and registers, per slab
     int64_t blob_bytes;
     unsigned *pub;         // [pop] per slab: the last level whose image it published (zero at launch)
     unsigned *got;         // [pop] per slab: receivers that have copied its image (zero at launch)
 };
+
+// Bytes of the whole-schedule kernel's level-end tables for a population.
+int64_t run_lend_bytes(int32_t pop);
 
 // Bytes of one hand-over image: the member's LDS region, then J, A and U of
 // every lane, the score, and J and A of the lanes' second row-shards.

@@ -1209,6 +1209,11 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
         run.blob_bytes = blob_bytes;
         run.pub = flags;
         run.got = flags + pop_size;
+        if (a.rv == 2) {  // the two-per-lane variant keeps its level-end tables in HBM
+            run.lend_stride = run_lend_bytes(pop_size);
+            run.lend = scr.get<char>((size_t)((pop_size + a.mpw - 1) / a.mpw) * (size_t)run.lend_stride);
+            if (scr.failed()) return ROUTEPACK_E_DEVICE;
+        }
         hipEvent_t e0 = nullptr, e1 = nullptr;
         if (prm->level_kernel_ms) {
             RP_HIP(hipEventCreate(&e0));

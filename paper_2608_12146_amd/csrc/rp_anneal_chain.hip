@@ -1359,7 +1359,10 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
     const int gw = blockIdx.x * a.mpw + wv;  // this wave's slab
     const bool active = gw < pop;
     const int nb = gridDim.x;
-    uint64_t *Fs = reinterpret_cast<uint64_t *>(smem + r.o_lend);
+    // level-end tables: in LDS, or (two row-shards per lane, whose member
+    // regions leave no room) in this workgroup's slice of r.lend
+    char *lend = GV == 2 ? r.lend + (int64_t)blockIdx.x * r.lend_stride : smem + r.o_lend;
+    uint64_t *Fs = reinterpret_cast<uint64_t *>(lend);
     int32_t *par = reinterpret_cast<int32_t *>(Fs + pop);
     int32_t *flag = par + pop;    // has-child flags, then the slab -> next member map
     int32_t *freed = flag + pop;  // slabs of members without children, ascending member
@@ -1711,15 +1714,17 @@ static int chain_launch_t(const AnnealArgs &a, hipStream_t stream) {
     return hipGetLastError() == hipSuccess ? ROUTEPACK_OK : ROUTEPACK_E_DEVICE;
 }
 
-// Level-end tables of the whole-schedule kernel (after the member regions).
-static int64_t run_lend_bytes(int32_t pop) { return 28 * (int64_t)pop; }
+// Level-end tables of the whole-schedule kernel (after the member regions,
+// or in HBM for the two-per-lane variant).
+int64_t run_lend_bytes(int32_t pop) { return (28 * (int64_t)pop + 255) & ~(int64_t)255; }
 
 template <int PV, int DV, int GV>
 static int chain_run_t(const AnnealArgs &a, const RunArgs &r0, int32_t n_cu, bool launch, hipStream_t stream) {
     RunArgs r = r0;
     if (a.mpw > kRunMaxWaves) return ROUTEPACK_E_UNSUPPORTED;
     const int64_t o_lend = ((int64_t)a.lds_shared + (int64_t)a.mpw * a.lds_member + 15) & ~(int64_t)15;
-    const int64_t lds = o_lend + run_lend_bytes(a.pop);
+    const int64_t lds = o_lend + (GV == 2 ? 0 : run_lend_bytes(a.pop));
+    if (GV == 2 && launch && (!r.lend || r.lend_stride < run_lend_bytes(a.pop))) return ROUTEPACK_E_INTERNAL;
     // static LDS of the kernel is below 1 KiB
     if (lds + 1024 > 160 * 1024) return ROUTEPACK_E_UNSUPPORTED;
     r.o_lend = (int32_t)o_lend;

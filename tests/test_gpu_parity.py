@@ -186,14 +186,14 @@ def _mid_oracle_levels(G=1):
 
 
 @gpu
-@pytest.mark.parametrize("kernel,G", [("chain_run", 1), ("chain", 1), ("wave", 1), ("chain", 2)])
+@pytest.mark.parametrize("kernel,G", [("chain_run", 1), ("chain", 1), ("wave", 1), ("chain_run", 2),
+                                      ("chain", 2)])
 def test_anneal_mid_sampled_levels(kernel, G, monkeypatch):
     """Mid window at its full population: two levels from the seeds, then one
     late level resumed from the GPU's population, each checked against the
     oracle on the same start states.  With G = 2 the row-shards (more than
-    64) take two per lane in the chain kernels; the whole-schedule kernel
-    does not fit there (its level-end tables would exceed the LDS), so the
-    per-level chain kernel is the default and is the one checked."""
+    64) take two per lane in the chain kernels, and the whole-schedule kernel
+    keeps its level-end tables in HBM."""
     import oracle as O
     rp = _rp()
     _use_kernel(monkeypatch, kernel)
