@@ -46,6 +46,12 @@ def kernel_sources(kernel):
     return [os.path.join(ROOT, "paper_2608_12146_amd", "csrc", f) for f in files]
 
 
+def config_tag(window, G=1, S=1):
+    """Name of a workload in profile file names: the window, plus the EDP
+    shard and stage counts when they are not 1."""
+    return window + (f"_g{G}" if G != 1 else "") + (f"_s{S}" if S != 1 else "")
+
+
 def pmc_file(kernel, window):
     return os.path.join(ROOT, "profiles", f"anneal_{kernel}_{window}_pmc.txt")
 
@@ -119,10 +125,11 @@ def read_lds(kernel, window, launch_ms):
         return None
 
 
-def workload_text(w, G):
+def workload_text(w, G, S=1):
     return (f"{w.name} window: {w.n} samples, {w.n_layers} layers x {w.n_experts} experts top-{w.top_k}, "
             f"{w.n_ranks} EP ranks, {w.n_dp} DP slots in {G} EDP shard(s), cap {w.capacity}, "
-            f"population {w.pop}, {w.levels} levels x 256 proposals")
+            + ("two attention stages (linear + quadratic), " if S == 2 else "")
+            + f"population {w.pop}, {w.levels} levels x 256 proposals")
 
 
 def copy_probe():
@@ -168,6 +175,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--window", default="mid")
     ap.add_argument("--edp", type=int, default=1, help="EDP shards G (contiguous slot blocks)")
+    ap.add_argument("--stages", type=int, default=1, choices=(1, 2),
+                    help="attention stages: 1, or 2 (a linear and a quadratic stage)")
     ap.add_argument("--levels", type=int, default=None, help="levels (default: the window's schedule)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-levels", type=int, default=300,
@@ -195,7 +204,7 @@ def main():
     from synth import windows as W
 
     w = synth.make_window(args.window, edp=args.edp)
-    pd = synth.window_problem(w)
+    pd = synth.window_problem(w, stages=args.stages)
     prob = rp.Problem.from_dict(pd)
     levels = args.levels or w.levels
     temps = synth.anneal_temperatures(w.levels)[:levels]
@@ -215,7 +224,7 @@ def main():
     def progress(msg):
         print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
-    progress(f"{workload_text(w, args.edp)}; levels {levels}")
+    progress(f"{workload_text(w, args.edp, args.stages)}; levels {levels}")
     for k in range(args.warmup):
         t1 = time.perf_counter()
         step()
@@ -247,8 +256,9 @@ def main():
     # the whole-schedule kernel is one launch per step; the others one per level
     launches = args.steps * (1 if level_kernel == "chain_run" else levels)
     achieved = evals * bytes_per_eval / k_sec / 1e9
-    traffic = read_pmc(level_kernel, args.window)
-    lds = read_lds(level_kernel, args.window, float(kms.sum()) / launches)
+    tag = config_tag(args.window, args.edp, args.stages)
+    traffic = read_pmc(level_kernel, tag)
+    lds = read_lds(level_kernel, tag, float(kms.sum()) / launches)
 
     # Objective == oracle: the oracle rescoring of the GPU's x*, the oracle's
     # seed population, and one level of three members recomputed by the oracle.
@@ -297,7 +307,7 @@ def main():
         "vs_baseline": None,
         "dtype": "int64",
         "data": "synthetic",
-        "config": {"workload": workload_text(w, args.edp), "levels": levels, "proposals_per_level": K},
+        "config": {"workload": workload_text(w, args.edp, args.stages), "levels": levels, "proposals_per_level": K},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": "k_anneal_" + level_kernel, "avg_launch_ms": float(kms.sum()) / launches,

@@ -61,6 +61,10 @@ WINDOWS = {
 FRAC_BITS = 12
 ALPHA_FP = 4096
 BETA_FP = 1
+# Two attention stages: a linear-attention stage (cost proportional to tokens,
+# a = 1, b = 0) and a quadratic one (a = 1/2, b = 1/4096), at 12 fractional bits.
+ALPHA_FP_2 = (4096, 2048)
+BETA_FP_2 = (0, 1)
 STEPS_PER_LEVEL = 256
 N_TRIALS = 16
 CHOICE_WIDTH = 4
@@ -265,11 +269,15 @@ def anneal_temperatures(levels: int, t_first: float = T_FIRST, t_last: float = T
     return t_first * (t_last / t_first) ** (n / (levels - 1))
 
 
-def window_problem(w: Window) -> dict:
-    """The scalar problem description shared by both implementations."""
+def window_problem(w: Window, stages: int = 1) -> dict:
+    """The scalar problem description shared by both implementations; stages
+    selects one attention stage or the two-stage (linear + quadratic) cost."""
+    assert stages in (1, 2)
+    alpha = [ALPHA_FP] if stages == 1 else list(ALPHA_FP_2)
+    beta = [BETA_FP] if stages == 1 else list(BETA_FP_2)
     return dict(n_samples=w.n, n_layers=w.n_layers, n_experts=w.n_experts,
                 top_k=w.top_k, n_ranks=w.n_ranks, n_dp=w.n_dp, n_edp=w.n_edp,
                 dp_to_edp=w.dp_to_edp.astype(np.int32), capacity=int(w.capacity),
-                alpha_fp=np.array([ALPHA_FP], dtype=np.int64),
-                beta_fp=np.array([BETA_FP], dtype=np.int64),
+                alpha_fp=np.array(alpha, dtype=np.int64),
+                beta_fp=np.array(beta, dtype=np.int64),
                 frac_bits=FRAC_BITS, min_rows=1)

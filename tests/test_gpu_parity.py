@@ -25,10 +25,10 @@ def _log(msg):
 
 
 @functools.lru_cache(maxsize=None)
-def _window(name, G=1):
+def _window(name, G=1, S=1):
     import oracle as O
     w = synth.make_window(name, edp=G)
-    pd = synth.window_problem(w)
+    pd = synth.window_problem(w, stages=S)
     pb = O.Problem.from_dict(pd)
     agg = O.aggregate(w.demand)
     slot, load = O.place(agg, w.n_ranks)
@@ -37,9 +37,9 @@ def _window(name, G=1):
 
 
 @functools.lru_cache(maxsize=None)
-def _packed(name, G=1):
+def _packed(name, G=1, S=1):
     import oracle as O
-    w, pd, pb, agg, slot, load, q = _window(name, G)
+    w, pd, pb, agg, slot, load, q = _window(name, G, S)
     pr = O.pack_rows(pb, w.lengths, q, w.seed_pack, synth.windows.N_TRIALS,
                      synth.windows.CHOICE_WIDTH, w.pop)
     assert pr["rc"] == 0
@@ -78,13 +78,14 @@ def test_aggregate_ragged_and_unaligned():
 
 
 @gpu
-@pytest.mark.parametrize("name,G", [("tiny", 1), ("tiny", 2), ("small", 1), ("small", 4), ("mid", 1)])
-def test_eval_objective(name, G):
+@pytest.mark.parametrize("name,G,S", [("tiny", 1, 1), ("tiny", 2, 1), ("small", 1, 1), ("small", 4, 1), ("mid", 1, 1),
+                                      ("tiny", 2, 2), ("small", 1, 2), ("mid", 1, 2)])
+def test_eval_objective(name, G, S):
     import oracle as O
     rp = _rp()
-    _log(f"eval_objective {name} G={G}")
-    w, pd, pb, agg, slot, load, q = _window(name, G)
-    pr = _packed(name, G)
+    _log(f"eval_objective {name} G={G} S={S}")
+    w, pd, pb, agg, slot, load, q = _window(name, G, S)
+    pr = _packed(name, G, S)
     R = pr["r_star"]
     lays = pr["population"][: min(w.pop, 32)].copy()
     # add infeasible layouts: an out-of-range id and an over-full cell
@@ -173,12 +174,36 @@ def test_anneal_small_levels(G, kernel, monkeypatch):
     _compare_anneal(g, o)
 
 
+@gpu
+@pytest.mark.parametrize("kernel", KERNELS)
+def test_anneal_two_stages(kernel, monkeypatch):
+    """Two attention stages (linear + quadratic): the full tiny schedule with
+    two EDP shards and 40 levels of small, on every annealing kernel."""
+    import oracle as O
+    rp = _rp()
+    _use_kernel(monkeypatch, kernel)
+    K = synth.windows.STEPS_PER_LEVEL
+    for name, G, nl in (("tiny", 2, None), ("small", 1, 40)):
+        w, pd, pb, agg, slot, load, q = _window(name, G, 2)
+        pr = _packed(name, G, 2)
+        full = synth.anneal_temperatures(w.levels)
+        temps = full if nl is None else full[:nl]
+        t_next = 0.0 if nl is None else full[nl]
+        _log(f"anneal {name} G={G} S=2, {len(temps)} levels, {kernel} kernel")
+        o = O.anneal(pb, w.lengths, q, pr["r_star"], pr["population"], temps, K, w.seed_anneal, t_next=t_next)
+        assert o["rc"] == 0
+        g = rp.anneal(rp.Problem.from_dict(pd), w.lengths, q, pr["r_star"], pr["population"], temps, K,
+                      w.seed_anneal, t_next=t_next)
+        assert g["level_kernel"] == kernel
+        _compare_anneal(g, o)
+
+
 @functools.lru_cache(maxsize=None)
-def _mid_oracle_levels(G=1):
+def _mid_oracle_levels(G=1, S=1):
     """Oracle levels 0-1 of the mid window from the seed population."""
     import oracle as O
-    w, pd, pb, agg, slot, load, q = _window("mid", G)
-    pr = _packed("mid", G)
+    w, pd, pb, agg, slot, load, q = _window("mid", G, S)
+    pr = _packed("mid", G, S)
     temps = synth.anneal_temperatures(w.levels)
     K = synth.windows.STEPS_PER_LEVEL
     return O.anneal(pb, w.lengths, q, pr["r_star"], pr["population"], temps[:2], K, w.seed_anneal,
@@ -186,9 +211,9 @@ def _mid_oracle_levels(G=1):
 
 
 @gpu
-@pytest.mark.parametrize("kernel,G", [("chain_run", 1), ("chain", 1), ("wave", 1), ("chain_run", 2),
-                                      ("chain", 2)])
-def test_anneal_mid_sampled_levels(kernel, G, monkeypatch):
+@pytest.mark.parametrize("kernel,G,S", [("chain_run", 1, 1), ("chain", 1, 1), ("wave", 1, 1), ("chain_run", 2, 1),
+                                        ("chain", 2, 1), ("chain_run", 1, 2)])
+def test_anneal_mid_sampled_levels(kernel, G, S, monkeypatch):
     """Mid window at its full population: two levels from the seeds, then one
     late level resumed from the GPU's population, each checked against the
     oracle on the same start states.  With G = 2 the row-shards (more than
@@ -197,18 +222,18 @@ def test_anneal_mid_sampled_levels(kernel, G, monkeypatch):
     import oracle as O
     rp = _rp()
     _use_kernel(monkeypatch, kernel)
-    w, pd, pb, agg, slot, load, q = _window("mid", G)
-    pr = _packed("mid", G)
+    w, pd, pb, agg, slot, load, q = _window("mid", G, S)
+    pr = _packed("mid", G, S)
     temps = synth.anneal_temperatures(w.levels)
     K = synth.windows.STEPS_PER_LEVEL
     prob = rp.Problem.from_dict(pd)
-    _log(f"anneal mid G={G} levels 0-1, {kernel} kernel ({pr['r_star'] * G} row-shards)")
-    o = _mid_oracle_levels(G)
+    _log(f"anneal mid G={G} S={S} levels 0-1, {kernel} kernel ({pr['r_star'] * G} row-shards)")
+    o = _mid_oracle_levels(G, S)
     g = rp.anneal(prob, w.lengths, q, pr["r_star"], pr["population"], temps[:2], K, w.seed_anneal,
                   t_next=temps[2])
     assert g["level_kernel"] == kernel
     _compare_anneal(g, o)
-    _log(f"anneal mid G={G} level 1500 resumed, {kernel} kernel")
+    _log(f"anneal mid G={G} S={S} level 1500 resumed, {kernel} kernel")
     start = g["population"].cpu().numpy()
     o2 = O.anneal(pb, w.lengths, q, pr["r_star"], start, temps[1500:1501], K, w.seed_anneal,
                   t_next=temps[1501], sweep_offset=1500, best_layout=o["best_layout"],
@@ -252,10 +277,10 @@ def test_anneal_crowded_cells(G, kernel, monkeypatch):
 
 
 @gpu
-@pytest.mark.parametrize("name,G", [("tiny", 1), ("tiny", 2), ("small", 1), ("small", 4),
-                                    ("mid", 1), ("mid", 2)])
+@pytest.mark.parametrize("name,G,S", [("tiny", 1, 1), ("tiny", 2, 1), ("small", 1, 1), ("small", 4, 1),
+                                      ("mid", 1, 1), ("mid", 2, 1), ("small", 2, 2), ("mid", 1, 2)])
 @pytest.mark.parametrize("path", ["default", "single"])
-def test_pack_rows(name, G, path, monkeypatch):
+def test_pack_rows(name, G, S, path, monkeypatch):
     """Row count and seed population equal to the oracle's; "single" requests
     the one-kernel seed trials, "default" the library's choice (three
     kernels where the shape allows)."""
@@ -264,9 +289,9 @@ def test_pack_rows(name, G, path, monkeypatch):
         monkeypatch.setenv("ROUTEPACK_PACK_KERNEL", "single")
     else:
         monkeypatch.delenv("ROUTEPACK_PACK_KERNEL", raising=False)
-    _log(f"pack_rows {name} G={G} ({path} seed trials)")
-    w, pd, pb, agg, slot, load, q = _window(name, G)
-    pr = _packed(name, G)
+    _log(f"pack_rows {name} G={G} S={S} ({path} seed trials)")
+    w, pd, pb, agg, slot, load, q = _window(name, G, S)
+    pr = _packed(name, G, S)
     g = rp.pack_rows(rp.Problem.from_dict(pd), w.lengths, q, w.seed_pack, synth.windows.N_TRIALS,
                      synth.windows.CHOICE_WIDTH, w.pop)
     assert (g["r_star"], g["certified"]) == (pr["r_star"], pr["certified"])
