@@ -61,8 +61,9 @@ WINDOWS = {
 FRAC_BITS = 12
 ALPHA_FP = 4096
 BETA_FP = 1
-# Two attention stages: a linear-attention stage (cost proportional to tokens,
-# a = 1, b = 0) and a quadratic one (a = 1/2, b = 1/4096), at 12 fractional bits.
+# Two attention stages (the KDA + MLA stack of Sec. 2.2): a linear stage
+# (a = 1, b = 0) and one with a quadratic term (a = 1/2, b = 1/4096), at 12
+# fractional bits.
 ALPHA_FP_2 = (4096, 2048)
 BETA_FP_2 = (0, 1)
 STEPS_PER_LEVEL = 256
