@@ -1663,7 +1663,9 @@ int chain_prepare(AnnealArgs &a, int32_t *qt, hipStream_t stream) {
 bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out, int32_t *dv_out) {
     const int32_t P = a.P;
     if (!(P == 4 || P == 8 || P == 16)) return false;
-    if (a.L > 32 || a.RG > 2 * kWave || max_count > 16 || a.N > 65535 || a.B + 1 > 65535 || a.C > 2147483647LL)
+    // (L >= 1: each move loads its rows with a layer on every lane of a half)
+    if (a.L < 1 || a.L > 32 || a.RG > 2 * kWave || max_count > 16 || a.N > 65535 || a.B + 1 > 65535 ||
+        a.C > 2147483647LL)
         return false;
     a.rv = a.RG > kWave ? 2 : 1;  // row-shards per lane
     const int32_t dv = max_count <= 8 ? 8 : 16;

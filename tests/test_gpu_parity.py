@@ -198,6 +198,54 @@ def test_anneal_two_stages(kernel, monkeypatch):
         _compare_anneal(g, o)
 
 
+# Degenerate shapes: no MoE layer (the rows are empty), a population that
+# fills no workgroup, a level size that is not a multiple of the batch of 64,
+# one DP slot, one proposal per level, and one row of two one-sample cells
+# (every relocation infeasible).
+DEGENERATE = {
+    "no_layers": (dict(n=40, layers=0, experts=4, top_k=2, ranks=4, dp=2, cap=200, pop=3, levels=6), 100),
+    "one_slot": (dict(n=24, layers=2, experts=8, top_k=2, ranks=4, dp=1, cap=300, pop=5, levels=8), 1),
+    "one_row": (dict(n=2, layers=2, experts=4, top_k=2, ranks=4, dp=2, cap=400, pop=2, levels=5), 64),
+}
+
+
+@gpu
+@pytest.mark.parametrize("kernel", KERNELS)
+@pytest.mark.parametrize("case", sorted(DEGENERATE))
+def test_anneal_degenerate_shapes(case, kernel, monkeypatch):
+    import oracle as O
+    rp = _rp()
+    _use_kernel(monkeypatch, kernel)
+    kw, K = DEGENERATE[case]
+    w = synth.make_tiny_random(70 + sorted(DEGENERATE).index(case), tmin=1, **kw)
+    pd = synth.window_problem(w)
+    pb = O.Problem.from_dict(pd)
+    slot, load = O.place(O.aggregate(w.demand), w.n_ranks)
+    q = O.project(w.demand, slot, w.n_ranks)
+    pr = O.pack_rows(pb, w.lengths, q, w.seed_pack, 8, 4, w.pop)
+    assert pr["rc"] == 0
+    if case == "one_row":
+        assert pr["r_star"] == 1
+    temps = synth.anneal_temperatures(w.levels)
+    if case == "no_layers" and kernel.startswith("chain"):
+        # the chain kernels need a layer per lane; the flat wave kernel takes this case
+        _log(f"anneal degenerate {case}: {kernel} kernel refuses")
+        with pytest.raises(rp.RoutepackError) as ei:
+            rp.anneal(rp.Problem.from_dict(pd), w.lengths, q, pr["r_star"], pr["population"], temps, K,
+                      w.seed_anneal)
+        assert ei.value.code == -8
+        monkeypatch.delenv("ROUTEPACK_ANNEAL_KERNEL")
+        kernel = "wave"
+    _log(f"anneal degenerate {case}: N={w.n} L={w.n_layers} D={w.n_dp} R*={pr['r_star']} pop={w.pop} "
+         f"K={K}, {kernel} kernel")
+    o = O.anneal(pb, w.lengths, q, pr["r_star"], pr["population"], temps, K, w.seed_anneal, want_steps=True)
+    assert o["rc"] == 0
+    g = rp.anneal(rp.Problem.from_dict(pd), w.lengths, q, pr["r_star"], pr["population"], temps, K,
+                  w.seed_anneal, want_steps=True)
+    assert g["level_kernel"] == kernel
+    _compare_anneal(g, o, steps=True)
+
+
 @functools.lru_cache(maxsize=None)
 def _mid_oracle_levels(G=1, S=1):
     """Oracle levels 0-1 of the mid window from the seed population."""
