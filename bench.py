@@ -279,6 +279,24 @@ def main():
     level_ok = bool(np.array_equal(g1["trace"].cpu().numpy()[0][ids], o1["trace"][0]))
 
     progress(f"parity: x* {score_ok}, pack {pack_ok}, level {level_ok}")
+
+    # QualityDiversitySelect on the window's canonical-distinct seeds: its own
+    # timing (the default step keeps the (score, discovery) seed order) and
+    # its order against the oracle's.
+    from oracle import qds
+    M = int(pk["n_distinct"])
+    cands = pk["population"][:M]
+    s0 = pk["scores"][:M, 0].contiguous()
+    sel_ms = []
+    for _ in range(6):
+        t1 = time.perf_counter()
+        sel = rp.select_population(prob, lengths, q, pk["r_star"], cands, s0, w.seed_pack, pop_size=w.pop)
+        sel_ms.append((time.perf_counter() - t1) * 1e3)
+    want = qds.select(pb, w.lengths, qn, opk["r_star"], opk["population"][:M], opk["scores"][:M, 0], w.seed_pack)
+    select = {"candidates": M, "ms_per_call": float(np.median(sel_ms[1:])),
+              "order_eq_oracle": sel["order"].cpu().tolist() == want.tolist()}
+    progress(f"select_population: {M} candidates, {select['ms_per_call']:.3f} ms, "
+             f"order == oracle {select['order_eq_oracle']}")
     cpu = None
     if not args.no_cpu_baseline:
         progress("cpu baseline (oracle)")
@@ -320,6 +338,7 @@ def main():
         "accept_rate": acc / max(evals, 1),
         "parity": {"x_star_score_eq_oracle": bool(score_ok), "pack_eq_oracle": bool(pack_ok),
                    "level0_sampled_members_eq_oracle": level_ok},
+        "select_population": select,
         "r_star": pk["r_star"],
         "best_score": an["best_score"].cpu().tolist(),
     }

@@ -218,6 +218,34 @@ int routepack_eval_objective(const routepack_problem *prob, const int32_t *lengt
                              int64_t *J, double *diag, const int64_t *rank_load,
                              hipStream_t stream);
 
+/* QualityDiversitySelect (Sec. 4.1.1, diverse fixed-row seeding; Alg. 2, the
+ * selection before the cyclic fill): the order in which canonical-distinct
+ * candidate layouts enter the seed population.  Starting from candidate 0
+ * (the exact-score winner), each step adds the candidate with the largest
+ * min over chosen y of d(x, y) minus the primary-score gap
+ * (s0(x) - s0(x_0)) / s0(x_0), the lower index on a tie, where
+ * d = (A / N + B / N + E / (8 R 2^20)) / 3: A and B count the samples whose
+ * cell, resp. row, holds a different sample set, and E is the L1 distance of
+ * the row-feature sketches -- the 2 + L row features (token sum over D C,
+ * sum of squared lengths over D C^2, and per layer sum_g max_p W over k D C,
+ * floored in 20-bit fixed point) projected on 8 sign vectors (the bits of
+ * Philox4x64-10 blocks (k, 0, 0, 4) under key (seed, 0)) and sorted over
+ * the rows.  All arithmetic is integer, so the order is exact.
+ *   candidates  int32 [n_cand][N]: layouts for R rows in (score, discovery)
+ *               order, 1 <= n_cand <= 64
+ *   primary     int64 [n_cand]: s0 of each candidate
+ *   order       int32 [n_cand] out: the selection order (order[0] = 0)
+ *   population  int32 [pop_size][N] out or NULL when pop_size = 0: the
+ *               candidates in that order, repeated
+ * Synchronizes.  E_LAYOUT when a candidate holds an id outside [0, R D), an
+ * empty cell or a cell over capacity; E_UNSUPPORTED when N or R D exceeds
+ * 65535, R exceeds 4096 or L exceeds 254; E_OVERFLOW when D C^2 >= 2^62. */
+int routepack_select_population(const routepack_problem *prob, const int32_t *lengths,
+                                const int32_t *q, int32_t n_rows, int32_t n_cand,
+                                const int32_t *candidates, const int64_t *primary, uint64_t seed,
+                                int32_t pop_size, int32_t *order, int32_t *population,
+                                hipStream_t stream);
+
 /* Human-readable name of a status code. */
 const char *routepack_strerror(int code);
 

@@ -23,7 +23,8 @@ ERRORS = {0: "ok", -1: "invalid argument", -2: "infeasible window", -3: "FixedRo
 LEVEL_KERNELS = {0: "workgroup", 1: "wave", 2: "chain", 3: "chain_run"}
 
 EXPORTS = ("routepack_aggregate_demand", "routepack_place_experts", "routepack_pack_rows",
-           "routepack_anneal", "routepack_eval_objective", "routepack_strerror")
+           "routepack_anneal", "routepack_eval_objective", "routepack_select_population",
+           "routepack_strerror")
 # measurement aid declared in include/routepack_probe.h (not part of the method)
 PROBE_EXPORTS = ("routepack_probe_lds_read",)
 
@@ -69,6 +70,7 @@ def load_library():
         lib.routepack_anneal.argtypes = [P, vp, vp, i32, i32, vp, C.POINTER(_AnnealParams), vp, vp,
                                          vp, vp, vp, vp]
         lib.routepack_eval_objective.argtypes = [P, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp]
+        lib.routepack_select_population.argtypes = [P, vp, vp, i32, i32, vp, vp, u64, i32, vp, vp, vp]
         lib.routepack_probe_lds_read.argtypes = [i32, i32, vp, C.POINTER(C.c_double), C.POINTER(C.c_int64), vp]
         lib.routepack_probe_lds_read.restype = C.c_int
         lib.routepack_strerror.argtypes = [C.c_int]
@@ -247,3 +249,21 @@ def probe_lds_read(n_workgroups=2048, reps=8192):
            lib.routepack_probe_lds_read(int(n_workgroups), int(reps), _ptr(sink), C.byref(ms), C.byref(nbytes),
                                         _stream()))
     return int(nbytes.value), float(ms.value)
+
+
+def select_population(prob: Problem, lengths, q, n_rows, candidates, primary, seed, pop_size=0):
+    """QualityDiversitySelect (routepack_select_population): the selection
+    order of the candidates and, when pop_size > 0, the population they fill."""
+    torch = _torch()
+    lib = load_library()
+    t = _dev(lengths, torch.int32)
+    qq = _dev(q, torch.int32) if q is not None else None
+    cand = _dev(candidates, torch.int32)
+    s0 = _dev(primary, torch.int64)
+    M = cand.shape[0]
+    order = torch.empty(M, dtype=torch.int32, device="cuda")
+    pop = torch.empty((pop_size, prob.n_samples), dtype=torch.int32, device="cuda") if pop_size > 0 else None
+    _check("routepack_select_population",
+           lib.routepack_select_population(prob.ref, _ptr(t), _ptr(qq), int(n_rows), int(M), _ptr(cand), _ptr(s0),
+                                           C.c_uint64(seed), int(pop_size), _ptr(order), _ptr(pop), _stream()))
+    return {"order": order, "population": pop}

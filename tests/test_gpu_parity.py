@@ -471,3 +471,56 @@ def test_lds_probe_reads_what_it_claims():
     want = (total ^ (total >> np.uint64(32))).astype(np.uint32)
     got = sink.cpu().numpy().view(np.uint32).reshape(nwg, 256)
     assert np.array_equal(got, np.broadcast_to(want, (nwg, 256)))
+
+
+@gpu
+@pytest.mark.parametrize("name,G,S", [("tiny", 1, 1), ("small", 1, 1), ("small", 4, 1), ("mid", 1, 1), ("mid", 2, 1),
+                                      ("small", 2, 2)])
+def test_select_population(name, G, S):
+    """QualityDiversitySelect: the selection order and the population it fills
+    equal to the oracle's, on the seed candidates of each window."""
+    from oracle import qds
+    rp = _rp()
+    w, pd, pb, agg, slot, load, q = _window(name, G, S)
+    pr = _packed(name, G, S)
+    M = pr["n_distinct"]
+    cands = pr["population"][:M]
+    s0 = pr["scores"][:M, 0]
+    _log(f"select_population {name} G={G} S={S}: {M} candidates, R*={pr['r_star']}")
+    want = qds.select(pb, w.lengths, q, pr["r_star"], cands, s0, w.seed_pack)
+    got = rp.select_population(rp.Problem.from_dict(pd), w.lengths, q, pr["r_star"], cands, s0, w.seed_pack,
+                               pop_size=w.pop)
+    assert got["order"].cpu().tolist() == want.tolist()
+    assert np.array_equal(got["population"].cpu().numpy(), qds.population(cands, want, w.pop))
+
+
+@gpu
+def test_select_population_constructed_and_errors():
+    """Constructed candidate sets (a row-relabelled twin, a far worse score,
+    ties) and the layout checks."""
+    from oracle import qds
+    rp = _rp()
+    w, pd, pb, agg, slot, load, q = _window("small")
+    pr = _packed("small")
+    R, D = pr["r_star"], w.n_dp
+    x0 = pr["population"][0]
+    twin = np.roll(np.arange(R), 3)[x0 // D] * D + x0 % D
+    others = [pr["population"][m] for m in range(1, pr["n_distinct"])]
+    prob = rp.Problem.from_dict(pd)
+    for cands, s0 in (([x0, twin] + others[:3], [100, 100, 100, 100, 100]),
+                      ([x0, twin, twin] + others[:2], [100, 100, 100, 10**9, 100]),
+                      ([x0], [5])):
+        cands = np.stack(cands).astype(np.int32)
+        want = qds.select(pb, w.lengths, q, R, cands, np.array(s0), 11)
+        got = rp.select_population(prob, w.lengths, q, R, cands, s0, 11)
+        assert got["order"].cpu().tolist() == want.tolist()
+    bad = np.stack([x0, x0]).astype(np.int32)
+    bad[1, 0] = R * D                                  # id out of range
+    with pytest.raises(rp.RoutepackError) as ei:
+        rp.select_population(prob, w.lengths, q, R, bad, [1, 1], 11)
+    assert ei.value.code == -4
+    empty = np.stack([x0, x0]).astype(np.int32)
+    empty[1][empty[1] == 0] = 1                        # cell 0 emptied (cell 1 may also overflow)
+    with pytest.raises(rp.RoutepackError) as ei:
+        rp.select_population(prob, w.lengths, q, R, empty, [1, 1], 11)
+    assert ei.value.code == -4

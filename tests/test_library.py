@@ -19,7 +19,8 @@ def _declared(header="routepack.h"):
 def test_header_declares_the_boundary():
     assert _declared() == sorted(["routepack_aggregate_demand", "routepack_place_experts",
                                   "routepack_pack_rows", "routepack_anneal",
-                                  "routepack_eval_objective", "routepack_strerror"])
+                                  "routepack_eval_objective", "routepack_select_population",
+                                  "routepack_strerror"])
 
 
 def test_library_exports_every_declared_symbol():
