@@ -297,6 +297,18 @@ def main():
               "order_eq_oracle": sel["order"].cpu().tolist() == want.tolist()}
     progress(f"select_population: {M} candidates, {select['ms_per_call']:.3f} ms, "
              f"order == oracle {select['order_eq_oracle']}")
+
+    # The row-count lower bound (volume, cardinality, Martello-Toth L2): R*
+    # is the minimum when it reaches it.
+    from oracle import bounds
+    rb_ms = []
+    for _ in range(6):
+        t1 = time.perf_counter()
+        rb = rp.row_lower_bound(prob, lengths)
+        rb_ms.append((time.perf_counter() - t1) * 1e3)
+    row_bound = {"r_bound": rb[0], "cell_bound": rb[1], "ms_per_call": float(np.median(rb_ms[1:])),
+                 "eq_oracle": rb == bounds.row_lower_bound(w.lengths, w.capacity, w.n_dp),
+                 "r_star_minimal": pk["r_star"] == rb[0]}
     cpu = None
     if not args.no_cpu_baseline:
         progress("cpu baseline (oracle)")
@@ -339,6 +351,7 @@ def main():
         "parity": {"x_star_score_eq_oracle": bool(score_ok), "pack_eq_oracle": bool(pack_ok),
                    "level0_sampled_members_eq_oracle": level_ok},
         "select_population": select,
+        "row_lower_bound": row_bound,
         "r_star": pk["r_star"],
         "best_score": an["best_score"].cpu().tolist(),
     }

@@ -218,6 +218,22 @@ int routepack_eval_objective(const routepack_problem *prob, const int32_t *lengt
                              int64_t *J, double *diag, const int64_t *rank_load,
                              hipStream_t stream);
 
+/* Lower bound on the row count (Sec. 3.2, Eqs. token-capacity and
+ * min-row-count): R* from routepack_pack_rows is the minimum R_min whenever
+ * it equals this bound, which can exceed the R_lb that pack_rows certifies
+ * against.  K_bound, a lower bound on the cells of any layout, is the largest
+ * of the token volume ceil(sum t / C), the cardinality bounds
+ * ceil(#{t_i (k+1) > C} / k) for k >= 1 (no cell holds k + 1 samples longer
+ * than C / (k + 1)), and Martello and Toth's L2 (1990) over every threshold
+ * alpha in {0} and the lengths at most C / 2; R_bound = max(1, min_rows,
+ * ceil(K_bound / D)).
+ *   lengths     int32 [N] t_i in [1, C]
+ *   r_bound     [host] int32 out
+ *   cell_bound  [host] int64 out or NULL: K_bound
+ * Synchronizes.  E_INFEASIBLE when some t_i is outside [1, C]. */
+int routepack_row_lower_bound(const routepack_problem *prob, const int32_t *lengths, int32_t *r_bound,
+                              int64_t *cell_bound, hipStream_t stream);
+
 /* QualityDiversitySelect (Sec. 4.1.1, diverse fixed-row seeding; Alg. 2, the
  * selection before the cyclic fill): the order in which canonical-distinct
  * candidate layouts enter the seed population.  Starting from candidate 0

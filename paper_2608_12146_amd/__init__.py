@@ -24,7 +24,7 @@ LEVEL_KERNELS = {0: "workgroup", 1: "wave", 2: "chain", 3: "chain_run"}
 
 EXPORTS = ("routepack_aggregate_demand", "routepack_place_experts", "routepack_pack_rows",
            "routepack_anneal", "routepack_eval_objective", "routepack_select_population",
-           "routepack_strerror")
+           "routepack_row_lower_bound", "routepack_strerror")
 # measurement aid declared in include/routepack_probe.h (not part of the method)
 PROBE_EXPORTS = ("routepack_probe_lds_read",)
 
@@ -71,6 +71,7 @@ def load_library():
                                          vp, vp, vp, vp]
         lib.routepack_eval_objective.argtypes = [P, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp]
         lib.routepack_select_population.argtypes = [P, vp, vp, i32, i32, vp, vp, u64, i32, vp, vp, vp]
+        lib.routepack_row_lower_bound.argtypes = [P, vp, C.POINTER(C.c_int32), C.POINTER(C.c_int64), vp]
         lib.routepack_probe_lds_read.argtypes = [i32, i32, vp, C.POINTER(C.c_double), C.POINTER(C.c_int64), vp]
         lib.routepack_probe_lds_read.restype = C.c_int
         lib.routepack_strerror.argtypes = [C.c_int]
@@ -267,3 +268,15 @@ def select_population(prob: Problem, lengths, q, n_rows, candidates, primary, se
            lib.routepack_select_population(prob.ref, _ptr(t), _ptr(qq), int(n_rows), int(M), _ptr(cand), _ptr(s0),
                                            C.c_uint64(seed), int(pop_size), _ptr(order), _ptr(pop), _stream()))
     return {"order": order, "population": pop}
+
+
+def row_lower_bound(prob: Problem, lengths):
+    """(R_bound, K_bound) of routepack_row_lower_bound: R* is minimal when it
+    equals R_bound."""
+    torch = _torch()
+    lib = load_library()
+    t = _dev(lengths, torch.int32)
+    r, k = C.c_int32(0), C.c_int64(0)
+    _check("routepack_row_lower_bound", lib.routepack_row_lower_bound(prob.ref, _ptr(t), C.byref(r), C.byref(k),
+                                                                      _stream()))
+    return int(r.value), int(k.value)

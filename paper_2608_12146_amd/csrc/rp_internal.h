@@ -71,6 +71,9 @@ int64_t w_entry_bound(const routepack_problem *p, const WindowStats &ws);
 int overflow_check(const routepack_problem *p, int64_t n_rows, const WindowStats &ws,
                    bool w_as_int32);
 
+// sigma = the samples ordered by (-t, i) (rp_pack.hip).
+int rank_sort_desc(const int32_t *lengths, int32_t N, int32_t *sigma, hipStream_t stream);
+
 // Device copies of small per-problem tables.
 struct DeviceProblem {
     int32_t *slots = nullptr;   // [G][D]

@@ -1012,6 +1012,13 @@ __global__ void k_pack_fill(const int32_t *canon, const int64_t *scores, const i
 
 }  // namespace rp
 
+namespace rp {
+int rank_sort_desc(const int32_t *lengths, int32_t N, int32_t *sigma, hipStream_t stream) {
+    hipLaunchKernelGGL(k_rank_sort, dim3((N + 255) / 256), dim3(256), 0, stream, lengths, N, sigma);
+    return hipGetLastError() == hipSuccess ? ROUTEPACK_OK : ROUTEPACK_E_DEVICE;
+}
+}  // namespace rp
+
 using namespace rp;
 
 extern "C" int routepack_pack_rows(const routepack_problem *prob, const int32_t *lengths,

@@ -524,3 +524,49 @@ def test_select_population_constructed_and_errors():
     with pytest.raises(rp.RoutepackError) as ei:
         rp.select_population(prob, w.lengths, q, R, empty, [1, 1], 11)
     assert ei.value.code == -4
+
+
+@gpu
+@pytest.mark.parametrize("name", ["tiny", "small", "mid", "heavy", "stress"])
+def test_row_lower_bound_windows(name):
+    """The row and cell bounds equal to the oracle's on every window."""
+    from oracle import bounds
+    rp = _rp()
+    w = synth.make_window(name)
+    pd = synth.window_problem(w)
+    _log(f"row_lower_bound {name} (N={w.n})")
+    want = bounds.row_lower_bound(w.lengths, w.capacity, w.n_dp)
+    assert rp.row_lower_bound(rp.Problem.from_dict(pd), w.lengths) == want
+
+
+@gpu
+@pytest.mark.parametrize("seed", range(8))
+def test_row_lower_bound_certifies_what_pack_rows_cannot(seed):
+    """Lengths just above C/3 (at most two per cell) and a few above C/2:
+    FFD's row count exceeds R_lb, so pack_rows does not certify it, while the
+    cardinality and L2 bounds reach it; random tiny windows besides."""
+    import oracle as O
+    from oracle import bounds
+    rp = _rp()
+    rng = np.random.default_rng([13, seed])
+    D = int(rng.choice([1, 2, 4]))
+    n = int(rng.integers(4 * D, 16 * D))
+    w = synth.make_tiny_random(200 + seed, n=n, layers=1, experts=4, top_k=2, ranks=4, dp=D, cap=300,
+                               tmin=1, tmax=300)
+    t = w.lengths.copy()
+    if seed % 2 == 0:
+        t[:] = 101 + rng.integers(0, 20, size=n)           # (1/3, 0.4] of C: two per cell at most
+        t[: max(1, n // 8)] = 151 + rng.integers(0, 40, size=max(1, n // 8))
+    pd = synth.window_problem(w)
+    pb = O.Problem.from_dict(pd)
+    want = bounds.row_lower_bound(t, w.capacity, D)
+    got = rp.row_lower_bound(rp.Problem.from_dict(pd), t)
+    _log(f"row_lower_bound seed {seed}: N={n} D={D} -> {got}")
+    assert got == want
+    q = np.zeros((n, 1, 4), dtype=np.int32)
+    q[:, 0, 0] = 2 * t                                      # any demand with sum_p q = k t
+    o = O.pack_rows(pb, t, q, 1, 2, 1, 2)
+    assert o["rc"] == 0
+    assert o["r_star"] == got[0]                            # the bound reaches FFD's row count
+    if seed % 2 == 0:
+        assert not o["certified"]                           # where R_lb falls short
