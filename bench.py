@@ -309,6 +309,21 @@ def main():
     row_bound = {"r_bound": rb[0], "cell_bound": rb[1], "ms_per_call": float(np.median(rb_ms[1:])),
                  "eq_oracle": rb == bounds.row_lower_bound(w.lengths, w.capacity, w.n_dp),
                  "r_star_minimal": pk["r_star"] == rb[0]}
+
+    # The fixed-bin search at the bound's row count: feasible there means the
+    # bound is R_min whatever FFD found.
+    from oracle import fixedbin
+    fb_ms = []
+    for _ in range(4):
+        t1 = time.perf_counter()
+        fb = rp.fixed_bin_search(prob, lengths, rb[0], 10 ** 6)
+        fb_ms.append((time.perf_counter() - t1) * 1e3)
+    fw = fixedbin.search(w.lengths, w.capacity, rb[0] * w.n_dp, 10 ** 6)
+    search = {"n_rows": rb[0], "status": fb[0], "nodes": fb[1], "ms_per_call": float(np.median(fb_ms[1:])),
+              "eq_oracle": fb[:2] == fw[:2] and (fb[2] is None) == (fw[2] is None)
+              and (fb[2] is None or np.array_equal(fb[2].cpu().numpy(), fw[2]))}
+    progress(f"fixed_bin_search at R={rb[0]}: status {fb[0]}, {fb[1]} nodes, {search['ms_per_call']:.3f} ms, "
+             f"== oracle {search['eq_oracle']}")
     cpu = None
     if not args.no_cpu_baseline:
         progress("cpu baseline (oracle)")
@@ -352,6 +367,7 @@ def main():
                    "level0_sampled_members_eq_oracle": level_ok},
         "select_population": select,
         "row_lower_bound": row_bound,
+        "fixed_bin_search": search,
         "r_star": pk["r_star"],
         "best_score": an["best_score"].cpu().tolist(),
     }

@@ -234,6 +234,30 @@ int routepack_eval_objective(const routepack_problem *prob, const int32_t *lengt
 int routepack_row_lower_bound(const routepack_problem *prob, const int32_t *lengths, int32_t *r_bound,
                               int64_t *cell_bound, hipStream_t stream);
 
+/* The fixed-bin feasibility check (Sec. 3.2, Eq. min-row-count): is there a
+ * layout with R rows (Eqs. sample-bijection, nonempty-cell, token-capacity
+ * with K = R D cells)?  Depth-first branch and bound in a fixed order, so the
+ * verdict, the node count and the first solution are defined: samples in
+ * (-t, i) order go to an open cell with room, lowest index first, then to
+ * the first unopened cell; a sample as long as the previous one goes to no
+ * lower cell; a branch is cut when fewer samples remain than unopened cells;
+ * a node is one placement.  Run it for R from routepack_row_lower_bound up
+ * to R* - 1: the first R found feasible is R_min, and if every one is
+ * infeasible, R* is.
+ *   n_rows       R
+ *   node_budget  placements allowed (>= 0)
+ *   status       [host] int32 out: 1 feasible, 0 infeasible, 2 unknown
+ *                (budget spent)
+ *   nodes        [host] int64 out or NULL: placements made
+ *   layout       int32 [N] out or NULL: the cell of each sample in the
+ *                first solution (written only when feasible)
+ * Synchronizes.  A sample over capacity, or more cells than samples, is
+ * infeasible (status 0, no node).  E_UNSUPPORTED when 8 (R D + N) bytes
+ * exceed 150 KiB of LDS. */
+int routepack_fixed_bin_search(const routepack_problem *prob, const int32_t *lengths, int32_t n_rows,
+                               int64_t node_budget, int32_t *status, int64_t *nodes, int32_t *layout,
+                               hipStream_t stream);
+
 /* QualityDiversitySelect (Sec. 4.1.1, diverse fixed-row seeding; Alg. 2, the
  * selection before the cyclic fill): the order in which canonical-distinct
  * candidate layouts enter the seed population.  Starting from candidate 0

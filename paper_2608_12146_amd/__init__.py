@@ -24,7 +24,7 @@ LEVEL_KERNELS = {0: "workgroup", 1: "wave", 2: "chain", 3: "chain_run"}
 
 EXPORTS = ("routepack_aggregate_demand", "routepack_place_experts", "routepack_pack_rows",
            "routepack_anneal", "routepack_eval_objective", "routepack_select_population",
-           "routepack_row_lower_bound", "routepack_strerror")
+           "routepack_row_lower_bound", "routepack_fixed_bin_search", "routepack_strerror")
 # measurement aid declared in include/routepack_probe.h (not part of the method)
 PROBE_EXPORTS = ("routepack_probe_lds_read",)
 
@@ -72,6 +72,8 @@ def load_library():
         lib.routepack_eval_objective.argtypes = [P, vp, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp]
         lib.routepack_select_population.argtypes = [P, vp, vp, i32, i32, vp, vp, u64, i32, vp, vp, vp]
         lib.routepack_row_lower_bound.argtypes = [P, vp, C.POINTER(C.c_int32), C.POINTER(C.c_int64), vp]
+        lib.routepack_fixed_bin_search.argtypes = [P, vp, i32, i64, C.POINTER(C.c_int32), C.POINTER(C.c_int64), vp,
+                                                   vp]
         lib.routepack_probe_lds_read.argtypes = [i32, i32, vp, C.POINTER(C.c_double), C.POINTER(C.c_int64), vp]
         lib.routepack_probe_lds_read.restype = C.c_int
         lib.routepack_strerror.argtypes = [C.c_int]
@@ -280,3 +282,17 @@ def row_lower_bound(prob: Problem, lengths):
     _check("routepack_row_lower_bound", lib.routepack_row_lower_bound(prob.ref, _ptr(t), C.byref(r), C.byref(k),
                                                                       _stream()))
     return int(r.value), int(k.value)
+
+
+def fixed_bin_search(prob: Problem, lengths, n_rows, node_budget):
+    """routepack_fixed_bin_search: (status, nodes, layout or None); status 1
+    feasible, 0 infeasible, 2 unknown."""
+    torch = _torch()
+    lib = load_library()
+    t = _dev(lengths, torch.int32)
+    lay = torch.full((prob.n_samples,), -1, dtype=torch.int32, device="cuda")
+    st, nodes = C.c_int32(0), C.c_int64(0)
+    _check("routepack_fixed_bin_search",
+           lib.routepack_fixed_bin_search(prob.ref, _ptr(t), int(n_rows), int(node_budget), C.byref(st),
+                                          C.byref(nodes), _ptr(lay), _stream()))
+    return int(st.value), int(nodes.value), (lay if st.value == 1 else None)

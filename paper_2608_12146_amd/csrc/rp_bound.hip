@@ -11,6 +11,18 @@
 //                     and L2 at alpha = the u-th length when it is at most
 //                     C / 2 (thread 0 also alpha = 0 and the volume); the
 //                     largest goes to one atomic maximum.
+// And the fixed-bin feasibility check itself (Eq. min-row-count: is the
+// feasible set X_R non-empty?) as a depth-first branch and bound under a
+// node budget, in a fixed order so that its verdict, node count and first
+// solution are defined:
+//   k_fixed_bin       one wave: samples in (-t, i) order go to an open cell
+//                     with room, lowest index first (a 64-lane ballot per
+//                     64 cells), then to the first unopened cell; a sample
+//                     equal in length to the previous one goes to no lower
+//                     cell; a branch is cut when fewer samples remain than
+//                     unopened cells.  Every iteration places a sample
+//                     (counted against the budget) or undoes one, so the
+//                     loop ends within twice the budget plus N iterations.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -94,6 +106,79 @@ __global__ void k_cell_bounds(const int64_t *ts, const int64_t *ps, int32_t N, i
     atomicMax(best, (unsigned long long)v);
 }
 
+__global__ void __launch_bounds__(kWave) k_fixed_bin(const int32_t *t, const int32_t *sigma, int32_t n, int64_t C,
+                                                     int32_t K, int64_t budget, int64_t *out, int32_t *cells) {
+    extern __shared__ __align__(16) char smem[];
+    int64_t *load = reinterpret_cast<int64_t *>(smem);       // [K]
+    int32_t *choice = reinterpret_cast<int32_t *>(load + K);  // [n] cell of sample h, -1 none
+    int32_t *ts = choice + n;                                 // [n] lengths in (-t, i) order
+    const int lane = lane_id();
+    for (int32_t c = lane; c < K; c += kWave) load[c] = 0;
+    for (int32_t u = lane; u < n; u += kWave) {
+        ts[u] = t[sigma[u]];
+        choice[u] = -1;
+    }
+    __syncthreads();
+    int32_t h = 0, opened = 0;
+    int64_t nodes = 0, status = 0;
+    for (;;) {
+        if (h == n) {  // every sample placed; the cut leaves no cell unopened
+            status = 1;
+            break;
+        }
+        const int64_t th = ts[h];
+        const int32_t ch = choice[h];
+        int32_t lo = ch + 1;
+        if (ch < 0 && h > 0 && th == ts[h - 1]) lo = choice[h - 1];
+        int32_t b = -1;
+        for (int32_t base = lo; base < opened && b < 0; base += kWave) {
+            const int32_t c = base + lane;
+            const uint64_t fit = __ballot(c < opened && load[c] + th <= C);
+            if (fit) b = base + first_lane(fit);
+        }
+        if (b < 0 && lo <= opened && opened < K) b = opened;
+        if (b >= 0) {
+            if (nodes == budget) {  // the next placement would exceed the budget
+                status = 2;
+                break;
+            }
+            ++nodes;
+            const bool fresh = b == opened;
+            opened += fresh ? 1 : 0;
+            if (lane == 0) {
+                load[b] += th;
+                choice[h] = b;
+            }
+            __syncthreads();
+            if (n - (h + 1) >= K - opened) {
+                ++h;
+                continue;  // (choice[h] is -1: set at the start, reset when left)
+            }
+            if (lane == 0) load[b] -= th;  // cut: undo, then the next cell for h
+            __syncthreads();
+            opened -= fresh ? 1 : 0;
+            continue;
+        }
+        // backtrack: sample h has no cell left
+        if (lane == 0) choice[h] = -1;
+        __syncthreads();
+        if (--h < 0) {
+            status = 0;
+            break;
+        }
+        const int32_t pb = choice[h];
+        if (lane == 0) load[pb] -= ts[h];
+        __syncthreads();
+        if (load[pb] == 0) --opened;  // it was the last cell opened
+    }
+    if (lane == 0) {
+        out[0] = status;
+        out[1] = nodes;
+    }
+    if (status == 1 && cells)
+        for (int32_t u = lane; u < n; u += kWave) cells[sigma[u]] = choice[u];
+}
+
 }  // namespace
 }  // namespace rp
 
@@ -131,5 +216,43 @@ extern "C" int routepack_row_lower_bound(const routepack_problem *prob, const in
     if (prob->min_rows > r) r = prob->min_rows;
     *r_bound = (int32_t)r;
     if (cell_bound) *cell_bound = (int64_t)k;
+    return ROUTEPACK_OK;
+}
+
+extern "C" int routepack_fixed_bin_search(const routepack_problem *prob, const int32_t *lengths, int32_t n_rows,
+                                          int64_t node_budget, int32_t *status, int64_t *nodes, int32_t *layout,
+                                          hipStream_t stream) {
+    Topology topo;
+    RP_TRY(check_problem(prob, &topo));
+    if (!lengths || !status || n_rows < 1 || node_budget < 0) return ROUTEPACK_E_INVALID;
+    const int32_t N = prob->n_samples;
+    const int64_t C = prob->capacity, K64 = (int64_t)n_rows * topo.D;
+    WindowStats ws;
+    RP_TRY(window_stats(prob, lengths, nullptr, &ws, stream));
+    if (ws.min_t < 1) return ROUTEPACK_E_INVALID;
+    if (K64 > N || ws.max_t > C) {  // no layout: more cells than samples, or a sample over capacity
+        *status = 0;
+        if (nodes) *nodes = 0;
+        return ROUTEPACK_OK;
+    }
+    const int32_t K = (int32_t)K64;
+    const size_t lds = 8 * (size_t)K + 8 * (size_t)N;
+    if (lds > 150 * 1024) return ROUTEPACK_E_UNSUPPORTED;
+    Scratch scr(stream);
+    int32_t *sigma = scr.get<int32_t>(N);
+    int64_t *out = scr.get<int64_t>(2);
+    if (scr.failed()) return ROUTEPACK_E_DEVICE;
+    RP_TRY(rank_sort_desc(lengths, N, sigma, stream));
+    if (hipFuncSetAttribute((const void *)k_fixed_bin, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
+        hipSuccess)
+        return ROUTEPACK_E_DEVICE;
+    hipLaunchKernelGGL(k_fixed_bin, dim3(1), dim3(kWave), lds, stream, lengths, (const int32_t *)sigma, N, C, K,
+                       node_budget, out, layout);
+    RP_HIP(hipGetLastError());
+    int64_t h[2] = {0, 0};
+    RP_HIP(hipMemcpyAsync(h, out, sizeof(h), hipMemcpyDeviceToHost, stream));
+    RP_HIP(hipStreamSynchronize(stream));
+    *status = (int32_t)h[0];
+    if (nodes) *nodes = h[1];
     return ROUTEPACK_OK;
 }

@@ -570,3 +570,109 @@ def test_row_lower_bound_certifies_what_pack_rows_cannot(seed):
     assert o["r_star"] == got[0]                            # the bound reaches FFD's row count
     if seed % 2 == 0:
         assert not o["certified"]                           # where R_lb falls short
+
+
+def _search_problem(rp, n, D, C, seed=0):
+    w = synth.make_tiny_random(300 + seed, n=n, layers=1, experts=4, top_k=2, ranks=4, dp=D, cap=C, tmin=1, tmax=C)
+    return rp.Problem.from_dict(synth.window_problem(w))
+
+
+def _check_search(rp, pb, t, C, D, R, budget):
+    """Verdict, node count and first solution equal to the oracle's; a
+    feasible layout is checked against the constraints as well."""
+    from oracle import fixedbin
+    want = fixedbin.search(t, C, R * D, budget)
+    got = rp.fixed_bin_search(pb, t, R, budget)
+    assert got[:2] == want[:2]
+    if want[0] == 1:
+        cells = got[2].cpu().numpy()
+        assert np.array_equal(cells, want[2])
+        load = np.bincount(cells, weights=np.asarray(t, dtype=np.int64), minlength=R * D)
+        assert len(load) == R * D and load.min() > 0 and load.max() <= C
+    else:
+        assert got[2] is None
+    return got[:2]
+
+
+@gpu
+@pytest.mark.parametrize("seed", range(40))
+def test_fixed_bin_search_matches_oracle(seed):
+    """Random lengths in [C/5, 3C/4) at the cell bound and one above it: proofs
+    of infeasibility, solutions after backtracking and budgets that run out
+    all give the oracle's verdict, node count and layout."""
+    from oracle import bounds
+    rp = _rp()
+    rng = np.random.default_rng([17, seed])
+    C = int(rng.integers(50, 400))
+    n = int(rng.integers(6, 40))
+    t = rng.integers(max(1, C // 5), C // 2 + C // 4, size=n).astype(np.int32)
+    pb = _search_problem(rp, n, 1, C, seed)
+    kb = bounds.cell_lower_bound(t, C)
+    for K in (kb, kb + 1):
+        for budget in (200000, int(rng.integers(0, 60))):
+            _log(f"fixed_bin_search seed {seed}: N={n} C={C} K={K} budget={budget}")
+            _check_search(rp, pb, t, C, 1, K, budget)
+
+
+@gpu
+@pytest.mark.parametrize("name", ["tiny", "small", "mid"])
+def test_fixed_bin_search_windows(name):
+    """At the row bound of each window the search finds the oracle's layout
+    (over 64 cells on small and mid: the ballot runs over several chunks)."""
+    from oracle import bounds
+    rp = _rp()
+    w = synth.make_window(name)
+    r, _ = bounds.row_lower_bound(w.lengths, w.capacity, w.n_dp)
+    _log(f"fixed_bin_search {name}: N={w.n} R={r}")
+    pb = rp.Problem.from_dict(synth.window_problem(w))
+    assert _check_search(rp, pb, w.lengths, w.capacity, w.n_dp, r, 10 ** 6)[0] == 1
+
+
+@gpu
+def test_fixed_bin_search_edges():
+    rp = _rp()
+    pb = _search_problem(rp, 9, 1, 100)
+    t = np.full(9, 34, dtype=np.int32)
+    assert _check_search(rp, pb, t, 100, 1, 4, 10 ** 6) == (0, 30)   # two 0.34 C per cell at most
+    assert _check_search(rp, pb, t, 100, 1, 5, 10 ** 6) == (1, 9)
+    assert rp.fixed_bin_search(pb, t, 10, 10) == (0, 0, None)          # more cells than samples
+    assert rp.fixed_bin_search(pb, t, 5, 0) == (2, 0, None)            # no placement allowed
+    assert rp.fixed_bin_search(pb, t, 5, 8) == (2, 8, None)            # one short
+    t2 = t.copy()
+    t2[3] = 101
+    assert rp.fixed_bin_search(pb, t2, 5, 100) == (0, 0, None)         # a sample over capacity
+    pb1 = _search_problem(rp, 1, 1, 100)
+    assert _check_search(rp, pb1, np.array([100], dtype=np.int32), 100, 1, 1, 1) == (1, 1)
+    for bad in ((t, 0, 10), (t, 1, -1)):
+        with pytest.raises(rp.RoutepackError) as ei:
+            rp.fixed_bin_search(pb, *bad)
+        assert ei.value.code == -1
+    t3 = t.copy()
+    t3[0] = 0
+    with pytest.raises(rp.RoutepackError) as ei:                       # a length below 1
+        rp.fixed_bin_search(pb, t3, 5, 10)
+    assert ei.value.code == -1
+    big = _search_problem(rp, 20000, 1, 100)
+    with pytest.raises(rp.RoutepackError) as ei:                       # 8 (K + N) bytes over 150 KiB
+        rp.fixed_bin_search(big, np.full(20000, 10, dtype=np.int32), 100, 10)
+    assert ei.value.code == -8
+
+
+@gpu
+@pytest.mark.parametrize("seed", range(0, 8, 2))
+def test_fixed_bin_search_closes_the_row_gap(seed):
+    """Where FFD's row count R* sits above every bound, the search over
+    R = R_bound .. R* - 1 takes the same verdicts as the oracle's: the first
+    feasible R is R_min, and R* is minimal when all are infeasible."""
+    from oracle import bounds
+    rp = _rp()
+    rng = np.random.default_rng([13, seed])
+    D = int(rng.choice([1, 2, 4]))
+    n = int(rng.integers(4 * D, 16 * D))
+    t = (101 + rng.integers(0, 20, size=n)).astype(np.int32)
+    t[: max(1, n // 8)] = 151 + rng.integers(0, 40, size=max(1, n // 8))
+    pb = _search_problem(rp, n, D, 300, seed)
+    r, _ = bounds.row_lower_bound(t, 300, D)
+    for R in range(max(1, r - 1), r + 3):
+        _log(f"fixed_bin_search gap seed {seed}: N={n} D={D} R={R}")
+        _check_search(rp, pb, t, 300, D, R, 10 ** 5)

@@ -20,7 +20,8 @@ def test_header_declares_the_boundary():
     assert _declared() == sorted(["routepack_aggregate_demand", "routepack_place_experts",
                                   "routepack_pack_rows", "routepack_anneal",
                                   "routepack_eval_objective", "routepack_select_population",
-                                  "routepack_row_lower_bound", "routepack_strerror"])
+                                  "routepack_row_lower_bound", "routepack_fixed_bin_search",
+                                  "routepack_strerror"])
 
 
 def test_library_exports_every_declared_symbol():
