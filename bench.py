@@ -168,6 +168,73 @@ def occupancy(kernel, pop):
     return None
 
 
+DIAG_KEYS = ("cv_global", "s_ep", "t_ep", "eta_ep", "attention", "joint")
+
+
+def _diag(d):
+    """eval_objective's diagnostics as named metrics: CV_global, S_EP, T_EP,
+    eta_EP, the attention sum and the joint max_g U (normalised by C)."""
+    return {k: float(v) for k, v in zip(DIAG_KEYS, (d[0], d[1], d[2], d[3], d[4], d[5]))}
+
+
+def compare_planners(rp, w, pd, levels, t_first=None, t_last=None):
+    """Three planners on one window, all on the GPU path, scored by the same
+    diagnostics (Sec. 6.3): baseline = identity placement pi_l(e) = e with the
+    length-only FFD layout; reorder = LPT placement with that FFD layout;
+    routepack = LPT placement, Alg. 2 seeds and annealing for `levels` levels
+    of the window's schedule.  The FFD layout is x_length of a two-trial
+    packing: the later of its one or two distinct seeds (x_paired is kept
+    only when strictly better, and the population is ordered by score)."""
+    import torch
+    import synth
+    from synth import windows as W
+    prob = rp.Problem.from_dict(pd)
+    demand = torch.as_tensor(w.demand, device="cuda")
+    lengths = torch.as_tensor(w.lengths, device="cuda")
+    agg = rp.aggregate_demand(prob, demand)
+    ident = torch.arange(w.n_experts, dtype=torch.int32, device="cuda").repeat(w.n_layers, 1)
+    g_id, q_id = rp.project_demand(prob, agg, ident, demand)
+    _, g_lpt, q = rp.place_experts(prob, agg, demand)
+    ffd = rp.pack_rows(prob, lengths, q, w.seed_pack, 2, 1, 2)
+    R = ffd["r_star"]
+    x_ffd = ffd["population"][ffd["n_distinct"] - 1]
+    pk = rp.pack_rows(prob, lengths, q, w.seed_pack, W.N_TRIALS, W.CHOICE_WIDTH, w.pop)
+    temps = synth.anneal_temperatures(w.levels, t_first or W.T_FIRST, t_last or W.T_LAST)[:levels]
+    an = rp.anneal(prob, lengths, q, R, pk["population"], temps, W.STEPS_PER_LEVEL, w.seed_anneal,
+                   want_trace=False, want_parents=False)
+    rows = {}
+    for name, qq, g, x in (("baseline", q_id, g_id, x_ffd), ("reorder", q, g_lpt, x_ffd),
+                           ("routepack", q, g_lpt, an["best_layout"])):
+        ev = rp.eval_objective(prob, lengths, qq, R, x, rank_load=g, want_diag=True)
+        assert int(ev["status"][0]) == 0
+        rows[name] = _diag(ev["diag"][0].cpu().numpy())
+    return {"window": w.name, "n_rows": R, "levels": levels, **rows,
+            "layouts": {"ffd": x_ffd.cpu().numpy(), "routepack": an["best_layout"].cpu().numpy()}}
+
+
+def compare(windows, levels, t_first=None, t_last=None):
+    """One JSON line per window: the three planners' metrics and the change
+    from each to the next (X3: CV_global under LPT; X4: FFD to annealing)."""
+    import paper_2608_12146_amd as rp
+    import synth
+    for name in windows:
+        print(f"[compare] {name}: generating", file=sys.stderr, flush=True)
+        w = synth.make_window(name)
+        pd = synth.window_problem(w)
+        t1 = time.perf_counter()
+        r = compare_planners(rp, w, pd, levels or w.levels, t_first, t_last)
+        r["temperatures"] = [t_first or synth.windows.T_FIRST, t_last or synth.windows.T_LAST]
+        r.pop("layouts")
+        b, o, g = r["baseline"], r["reorder"], r["routepack"]
+        r["change"] = {
+            "cv_global_lpt": o["cv_global"] / b["cv_global"] - 1.0 if b["cv_global"] else None,
+            **{f"{k}_anneal": g[k] / o[k] - 1.0 if o[k] else None for k in DIAG_KEYS[1:]},
+        }
+        r["seconds"] = time.perf_counter() - t1
+        print(f"[compare] {name}: {r['seconds']:.1f} s", file=sys.stderr, flush=True)
+        print(json.dumps(r), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -183,6 +250,10 @@ def main():
                     help="levels in the oracle's timed sample (about 10-30 s on 16 host threads)")
     ap.add_argument("--copy-probe", action="store_true")
     ap.add_argument("--lds-probe", action="store_true")
+    ap.add_argument("--compare", default=None, metavar="WINDOWS",
+                    help="comma-separated windows: baseline / reorder / routepack metrics instead of the bench")
+    ap.add_argument("--t-first", type=float, default=None, help="--compare: first temperature of the schedule")
+    ap.add_argument("--t-last", type=float, default=None, help="--compare: last temperature of the schedule")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the planner path is "
@@ -197,6 +268,9 @@ def main():
         return
     if args.lds_probe:
         lds_probe()
+        return
+    if args.compare:
+        compare(args.compare.split(","), args.levels, args.t_first, args.t_last)
         return
 
     import paper_2608_12146_amd as rp

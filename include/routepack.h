@@ -98,6 +98,20 @@ int routepack_place_experts(const routepack_problem *prob, const int64_t *agg,
                             int32_t *slot_of, int64_t *rank_load,
                             const int32_t *demand, int32_t *q, hipStream_t stream);
 
+/* Rank loads and projected demand of a given placement (Sec. 3.3, Eqs.
+ * placement-load and physical-rank-demand), for a placement the caller keeps
+ * instead of LPT's, such as the identity pi_l(e) = e of a planner that does
+ * not reorder experts.
+ *   agg         int64 [L][E]          window aggregate
+ *   slot_of     int32 [L][E]          pi_l(e); each layer a permutation of [0, E)
+ *   rank_load   int64 [L][P]          out: G_{l,p}
+ *   demand, q   as in routepack_place_experts (q computed when both are given)
+ * Synchronizes (it checks slot_of first).  E_INVALID on null inputs or
+ * outputs, E % P != 0, or a layer of slot_of that is not a permutation (then
+ * nothing is written to q); E_UNSUPPORTED when 4 E bytes exceed the LDS. */
+int routepack_project_demand(const routepack_problem *prob, const int64_t *agg, const int32_t *slot_of,
+                             int64_t *rank_load, const int32_t *demand, int32_t *q, hipStream_t stream);
+
 /* Row count and seed population (Sec. 3.2 and Alg. 2).
  * R_lb = max(1, min_rows, ceil(sum t / (C D)), ceil(#{t_i > C/2} / D));
  * R* = the first R >= R_lb for which FixedRowFFD with R*D cells succeeds

@@ -151,6 +151,20 @@ def project(demand, slot_of, n_ranks):
     return q
 
 
+def placement_load(agg, slot_of, n_ranks):
+    """G_{l,p} = sum of agg[l][e] over the experts e with owner(pi_l(e)) = p,
+    owner(v) = v // H, H = E / P (Eq. placement-load), for any placement."""
+    a = np.asarray(agg, dtype=np.int64)
+    s = np.asarray(slot_of, dtype=np.int64)
+    L, E = a.shape
+    H = E // n_ranks
+    G = np.zeros((L, n_ranks), dtype=np.int64)
+    for l in range(L):
+        for e in range(E):
+            G[l, s[l, e] // H] += a[l, e]
+    return G
+
+
 def score(prob: Problem, lengths, q, n_rows, layout, rank_load=None, want_J=False, want_diag=False):
     """Exact fixed-point score of one layout (Eqs. 11-15) -> (status, s[3], J, diag)."""
     lib = _load()

@@ -24,7 +24,8 @@ LEVEL_KERNELS = {0: "workgroup", 1: "wave", 2: "chain", 3: "chain_run"}
 
 EXPORTS = ("routepack_aggregate_demand", "routepack_place_experts", "routepack_pack_rows",
            "routepack_anneal", "routepack_eval_objective", "routepack_select_population",
-           "routepack_row_lower_bound", "routepack_fixed_bin_search", "routepack_strerror")
+           "routepack_row_lower_bound", "routepack_fixed_bin_search", "routepack_project_demand",
+           "routepack_strerror")
 # measurement aid declared in include/routepack_probe.h (not part of the method)
 PROBE_EXPORTS = ("routepack_probe_lds_read",)
 
@@ -66,6 +67,7 @@ def load_library():
         P = C.POINTER(_Problem)
         lib.routepack_aggregate_demand.argtypes = [P, vp, vp, vp]
         lib.routepack_place_experts.argtypes = [P, vp, vp, vp, vp, vp, vp]
+        lib.routepack_project_demand.argtypes = [P, vp, vp, vp, vp, vp, vp]
         lib.routepack_pack_rows.argtypes = [P, vp, vp, u64, i32, i32, i32, vp, vp, vp, vp, vp, vp]
         lib.routepack_anneal.argtypes = [P, vp, vp, i32, i32, vp, C.POINTER(_AnnealParams), vp, vp,
                                          vp, vp, vp, vp]
@@ -165,6 +167,22 @@ def place_experts(prob: Problem, agg, demand=None):
     _check("routepack_place_experts", lib.routepack_place_experts(prob.ref, _ptr(a), _ptr(slot), _ptr(load),
                                                                    _ptr(d), _ptr(q), _stream()))
     return slot, load, q
+
+
+def project_demand(prob: Problem, agg, slot_of, demand=None):
+    """A given placement: returns (rank_load [L][P], q [N][L][P] or None)."""
+    torch = _torch()
+    lib = load_library()
+    a = _dev(agg, torch.int64)
+    s = _dev(slot_of, torch.int32)
+    load = torch.empty((prob.n_layers, prob.n_ranks), dtype=torch.int64, device="cuda")
+    d = None if demand is None else _dev(demand, torch.int32)
+    q = None
+    if d is not None:
+        q = torch.empty((prob.n_samples, prob.n_layers, prob.n_ranks), dtype=torch.int32, device="cuda")
+    _check("routepack_project_demand", lib.routepack_project_demand(prob.ref, _ptr(a), _ptr(s), _ptr(load),
+                                                                     _ptr(d), _ptr(q), _stream()))
+    return load, q
 
 
 def pack_rows(prob: Problem, lengths, q, seed, n_trials, width, pop):

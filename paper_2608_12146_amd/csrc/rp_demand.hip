@@ -156,9 +156,57 @@ __global__ void __launch_bounds__(256) k_project(const int32_t *__restrict__ dem
     }
 }
 
+// A given placement pi_l: checks that it is a permutation of the E slots (an
+// LDS inverse filled by compare-and-swap: no slot out of range and no slot
+// taken twice), writes the inverse for k_project and sums every rank's
+// aggregate (Eq. placement-load).  One workgroup per layer.
+__global__ void __launch_bounds__(256) k_given_place(const int64_t *__restrict__ agg,
+                                                     const int32_t *__restrict__ slot_of, int32_t E,
+                                                     int32_t P, int32_t *__restrict__ expert_at_slot,
+                                                     int64_t *__restrict__ rank_load, int32_t *bad) {
+    extern __shared__ char smem[];
+    int32_t *eas = reinterpret_cast<int32_t *>(smem);  // [E]
+    const int l = blockIdx.x;
+    for (int v = threadIdx.x; v < E; v += blockDim.x) eas[v] = -1;
+    __syncthreads();
+    bool ok = true;
+    for (int e = threadIdx.x; e < E; e += blockDim.x) {
+        const int32_t v = slot_of[(int64_t)l * E + e];
+        if (v < 0 || v >= E || atomicCAS(&eas[v], -1, e) != -1) ok = false;
+    }
+    if (!ok) atomicOr(bad, 1);
+    __syncthreads();
+    for (int v = threadIdx.x; v < E; v += blockDim.x) expert_at_slot[(int64_t)l * E + v] = eas[v];
+    const int32_t H = E / P;
+    for (int p = threadIdx.x; p < P; p += blockDim.x) {
+        int64_t sum = 0;
+        for (int h = 0; h < H; ++h) {
+            const int32_t e = eas[p * H + h];
+            sum += e >= 0 ? agg[(int64_t)l * E + e] : 0;
+        }
+        rank_load[(int64_t)l * P + p] = sum;
+    }
+}
+
 }  // namespace rp
 
 using namespace rp;
+
+namespace {
+
+int launch_project(const int32_t *demand, const int32_t *eas, int32_t *q, int32_t N, int32_t L, int32_t E,
+                   int32_t P, hipStream_t stream) {
+    int32_t tile = 8192 / E;
+    if (tile < 1) tile = 1;
+    if (tile > 64) tile = 64;
+    const size_t lds2 = (size_t)E * 4 + (size_t)tile * E * 4;
+    if (lds2 > 160 * 1024) return ROUTEPACK_E_UNSUPPORTED;
+    const unsigned gy = (unsigned)((N + tile - 1) / tile);
+    hipLaunchKernelGGL(k_project, dim3(L, gy), dim3(256), lds2, stream, demand, eas, q, N, L, E, P, tile);
+    return ROUTEPACK_OK;
+}
+
+}  // namespace
 
 extern "C" int routepack_aggregate_demand(const routepack_problem *prob, const int32_t *demand,
                                           int64_t *agg, hipStream_t stream) {
@@ -203,15 +251,30 @@ extern "C" int routepack_place_experts(const routepack_problem *prob, const int6
     if (lds > 160 * 1024) return ROUTEPACK_E_UNSUPPORTED;
     hipLaunchKernelGGL(k_lpt_place, dim3(L), dim3(64), lds, stream, agg, E, P, slot_of, rank_load,
                        eas);
-    if (want_q) {
-        int32_t tile = 8192 / E;
-        if (tile < 1) tile = 1;
-        if (tile > 64) tile = 64;
-        const size_t lds2 = (size_t)E * 4 + (size_t)tile * E * 4;
-        if (lds2 > 160 * 1024) return ROUTEPACK_E_UNSUPPORTED;
-        const unsigned gy = (unsigned)((N + tile - 1) / tile);
-        hipLaunchKernelGGL(k_project, dim3(L, gy), dim3(256), lds2, stream, demand, eas, q, N, L, E,
-                           P, tile);
-    }
+    if (want_q) RP_TRY(launch_project(demand, eas, q, N, L, E, P, stream));
+    return hipGetLastError() == hipSuccess ? ROUTEPACK_OK : ROUTEPACK_E_DEVICE;
+}
+
+extern "C" int routepack_project_demand(const routepack_problem *prob, const int64_t *agg,
+                                        const int32_t *slot_of, int64_t *rank_load, const int32_t *demand,
+                                        int32_t *q, hipStream_t stream) {
+    if (!prob || !agg || !slot_of || !rank_load) return ROUTEPACK_E_INVALID;
+    const int32_t L = prob->n_layers, E = prob->n_experts, P = prob->n_ranks, N = prob->n_samples;
+    if (L < 0 || E < 1 || P < 1 || E % P != 0 || N < 0) return ROUTEPACK_E_INVALID;
+    if (L == 0) return ROUTEPACK_OK;
+    if ((size_t)E * 4 > 160 * 1024) return ROUTEPACK_E_UNSUPPORTED;
+    Scratch scr(stream);
+    int32_t *eas = scr.get<int32_t>((size_t)L * E);
+    int32_t *bad = scr.get<int32_t>(1);
+    if (scr.failed()) return ROUTEPACK_E_DEVICE;
+    RP_HIP(hipMemsetAsync(bad, 0, sizeof(int32_t), stream));
+    hipLaunchKernelGGL(k_given_place, dim3(L), dim3(256), (size_t)E * 4, stream, agg, slot_of, E, P, eas,
+                       rank_load, bad);
+    RP_HIP(hipGetLastError());
+    int32_t h_bad = 0;
+    RP_HIP(hipMemcpyAsync(&h_bad, bad, sizeof(h_bad), hipMemcpyDeviceToHost, stream));
+    RP_HIP(hipStreamSynchronize(stream));
+    if (h_bad) return ROUTEPACK_E_INVALID;
+    if (demand && q && N > 0) RP_TRY(launch_project(demand, eas, q, N, L, E, P, stream));
     return hipGetLastError() == hipSuccess ? ROUTEPACK_OK : ROUTEPACK_E_DEVICE;
 }

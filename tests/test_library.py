@@ -20,7 +20,7 @@ def test_header_declares_the_boundary():
     assert _declared() == sorted(["routepack_aggregate_demand", "routepack_place_experts",
                                   "routepack_pack_rows", "routepack_anneal",
                                   "routepack_eval_objective", "routepack_select_population",
-                                  "routepack_row_lower_bound", "routepack_fixed_bin_search",
+                                  "routepack_row_lower_bound", "routepack_fixed_bin_search", "routepack_project_demand",
                                   "routepack_strerror"])
 
 

@@ -14,6 +14,7 @@ import numpy as np
 import pytest
 
 import synth
+import oracle as O
 from oracle import brute
 
 GOLD = os.path.join(os.path.dirname(__file__), "golden")
@@ -450,3 +451,27 @@ def test_anneal_rejects_bad_input(oracle_mod):
     bad[0, 0] = R * w.n_dp        # out-of-range cell
     assert oracle_mod.anneal(prob, w.lengths, q, R, bad, [1e-3], 8, 1)["rc"] == -4
     assert oracle_mod.anneal(prob, w.lengths, q, R, pr["population"], [1e-3, 2e-3], 8, 1)["rc"] == -1
+
+
+def test_placement_load_by_hand():
+    # E = 4 experts on P = 2 ranks (H = 2 slots each): identity keeps experts
+    # {0, 1} on rank 0; pi = (3, 0, 1, 2) puts experts 1 and 2 there.
+    agg = np.array([[5, 1, 7, 3]], dtype=np.int64)
+    assert O.placement_load(agg, np.array([[0, 1, 2, 3]]), 2).tolist() == [[6, 10]]
+    assert O.placement_load(agg, np.array([[3, 0, 1, 2]]), 2).tolist() == [[8, 8]]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_placement_load_matches_lpt_running_loads(seed):
+    """For LPT's placement the loads equal the running loads that LPT keeps
+    while it places (Alg. 1), and every layer's loads sum to its aggregate."""
+    rng = np.random.default_rng([19, seed])
+    P = int(rng.choice([1, 2, 4, 8]))
+    E = P * int(rng.integers(1, 6))
+    agg = rng.integers(0, 1000, size=(3, E)).astype(np.int64)
+    slot, load = O.place(agg, P)
+    G = O.placement_load(agg, slot, P)
+    assert np.array_equal(G, load)
+    assert np.array_equal(G.sum(axis=1), agg.sum(axis=1))
+    perm = np.stack([rng.permutation(E) for _ in range(3)])
+    assert np.array_equal(O.placement_load(agg, perm, P).sum(axis=1), agg.sum(axis=1))
