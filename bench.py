@@ -168,6 +168,48 @@ def occupancy(kernel, pop):
     return None
 
 
+def demand_stream(reps=10):
+    """The HBM stream of the path's first steps at the largest window shape
+    (32768 samples, 64 layers x 512 experts, 64 ranks: 4 GiB of int32
+    demand, seeded random counts): routepack_aggregate_demand (algorithmic
+    bytes N L E 4 read + L E 8 written) and routepack_place_experts (LPT and
+    the projection: N L E 4 read + N L P 4 written), each timed with HIP
+    events on the library's stream over `reps` calls."""
+    import torch
+    import paper_2608_12146_amd as rp
+    N, L, E, P = 32768, 64, 512, 64
+    g = torch.Generator(device="cuda")
+    g.manual_seed(2608)
+    d = torch.randint(0, 64, (N, L, E), dtype=torch.int32, device="cuda", generator=g)
+    prob = rp.Problem(N, L, E, 8, P, 1, 1, [0], 1 << 20, [4096], [1])
+    agg = rp.aggregate_demand(prob, d)
+    ok = bool(torch.equal(agg, d.sum(dim=0, dtype=torch.int64)))
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    s.record()
+    for _ in range(reps):
+        rp.aggregate_demand(prob, d)
+    e.record()
+    torch.cuda.synchronize()
+    ms_a = s.elapsed_time(e) / reps
+    rp.place_experts(prob, agg, d)
+    torch.cuda.synchronize()
+    s.record()
+    for _ in range(reps):
+        rp.place_experts(prob, agg, d)
+    e.record()
+    torch.cuda.synchronize()
+    ms_p = s.elapsed_time(e) / reps
+    ba, bp = N * L * E * 4 + L * E * 8, N * L * E * 4 + N * L * P * 4
+    del d
+    torch.cuda.empty_cache()
+    return {"shape": {"samples": N, "layers": L, "experts": E, "ranks": P},
+            "aggregate": {"ms_per_call": ms_a, "bytes": ba, "achieved_gbs": ba / ms_a / 1e6,
+                          "frac": ba / ms_a / 1e6 / HBM_PEAK_GBS, "eq_torch_sum": ok},
+            "place_and_project": {"ms_per_call": ms_p, "bytes": bp, "achieved_gbs": bp / ms_p / 1e6,
+                                  "frac": bp / ms_p / 1e6 / HBM_PEAK_GBS}}
+
+
 DIAG_KEYS = ("cv_global", "s_ep", "t_ep", "eta_ep", "attention", "joint")
 
 
@@ -250,6 +292,8 @@ def main():
                     help="levels in the oracle's timed sample (about 10-30 s on 16 host threads)")
     ap.add_argument("--copy-probe", action="store_true")
     ap.add_argument("--lds-probe", action="store_true")
+    ap.add_argument("--demand-probe", action="store_true",
+                    help="only the aggregation / projection HBM stream at the largest window shape")
     ap.add_argument("--compare", default=None, metavar="WINDOWS",
                     help="comma-separated windows: baseline / reorder / routepack metrics instead of the bench")
     ap.add_argument("--t-first", type=float, default=None, help="--compare: first temperature of the schedule")
@@ -268,6 +312,9 @@ def main():
         return
     if args.lds_probe:
         lds_probe()
+        return
+    if args.demand_probe:
+        print(json.dumps(demand_stream()), flush=True)
         return
     if args.compare:
         compare(args.compare.split(","), args.levels, args.t_first, args.t_last)
@@ -398,6 +445,9 @@ def main():
               and (fb[2] is None or np.array_equal(fb[2].cpu().numpy(), fw[2]))}
     progress(f"fixed_bin_search at R={rb[0]}: status {fb[0]}, {fb[1]} nodes, {search['ms_per_call']:.3f} ms, "
              f"== oracle {search['eq_oracle']}")
+    dstream = demand_stream()
+    progress(f"demand stream at 32768 x 64 x 512: aggregate {dstream['aggregate']['achieved_gbs']:.0f} GB/s, "
+             f"place+project {dstream['place_and_project']['achieved_gbs']:.0f} GB/s")
     cpu = None
     if not args.no_cpu_baseline:
         progress("cpu baseline (oracle)")
@@ -442,6 +492,7 @@ def main():
         "select_population": select,
         "row_lower_bound": row_bound,
         "fixed_bin_search": search,
+        "demand_stream": dstream,
         "r_star": pk["r_star"],
         "best_score": an["best_score"].cpu().tolist(),
     }

@@ -79,6 +79,12 @@ def test_project_demand_matches_oracle(seed):
     assert np.array_equal(q.cpu().numpy(), O.project(w.demand, slot, P))
     g2, q2 = rp.project_demand(prob, agg, slot)
     assert q2 is None and np.array_equal(g2.cpu().numpy(), g.cpu().numpy())
+    import torch
+    big = torch.zeros(w.demand.size + 1, dtype=torch.int32, device="cuda")
+    big[1:] = torch.as_tensor(w.demand.reshape(-1), device="cuda")
+    off = big[1:].view(w.demand.shape)                    # rows not 16-byte aligned
+    _, q3 = rp.project_demand(prob, agg, slot, off)
+    assert np.array_equal(q3.cpu().numpy(), q.cpu().numpy())
 
 
 @gpu

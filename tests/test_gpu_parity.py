@@ -70,11 +70,22 @@ def test_aggregate_place_project(name):
 def test_aggregate_ragged_and_unaligned():
     rp = _rp()
     rng = np.random.default_rng(0)
-    for (n, L, E) in [(1, 1, 1), (3, 5, 7), (1000, 3, 13), (257, 2, 6)]:
+    import torch
+    # ragged column counts, several column blocks and row bands (bands of at
+    # least 64 rows, four waves taking every fourth row), and rows that are
+    # not 16-byte aligned (the scalar path)
+    for (n, L, E) in [(1, 1, 1), (3, 5, 7), (1000, 3, 13), (257, 2, 6), (5000, 3, 100), (70, 4, 64),
+                      (131, 2, 512)]:
         d = rng.integers(0, 1000, size=(n, L, E)).astype(np.int32)
         prob = rp.Problem(n, L, E, 1, 1, 1, 1, [0], 10**6, [4096], [1])
+        want = d.sum(axis=0, dtype=np.int64)
         g = rp.aggregate_demand(prob, d)
-        assert np.array_equal(g.cpu().numpy(), d.sum(axis=0, dtype=np.int64))
+        assert np.array_equal(g.cpu().numpy(), want)
+        big = torch.zeros(d.size + 1, dtype=torch.int32, device="cuda")
+        big[1:] = torch.as_tensor(d.reshape(-1), device="cuda")
+        off = big[1:].view(n, L, E)                       # 4 bytes past a 16-byte boundary
+        assert off.data_ptr() % 16 != 0
+        assert np.array_equal(rp.aggregate_demand(prob, off).cpu().numpy(), want)
 
 
 @gpu
