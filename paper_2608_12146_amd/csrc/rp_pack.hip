@@ -727,7 +727,7 @@ __global__ void __launch_bounds__(128) k_pack_cellsum(TrialArgs a, PackFast pf) 
 }
 
 // EDPAwarePair of candidate b (block per candidate).
-__global__ void __launch_bounds__(256) k_pack_pair(TrialArgs a, PackFast pf) {
+__global__ void __launch_bounds__(1024) k_pack_pair(TrialArgs a, PackFast pf) {
     extern __shared__ __align__(16) char spair[];
     __shared__ int32_t s_h;
     const int b = blockIdx.x, tid = threadIdx.x, nt = blockDim.x, lane = lane_id(), wv = wave_id();
@@ -767,7 +767,7 @@ __global__ void __launch_bounds__(256) k_pack_pair(TrialArgs a, PackFast pf) {
     __syncthreads();
     for (int32_t e = tid; e < LP; e += nt) qb[e] = Qc[(int64_t)order[0] * LP + e];
     __syncthreads();
-    constexpr int kPre = 16;  // Q entries per thread held for the next step (LP <= 16 * 256)
+    constexpr int kPre = 16;  // Q entries per thread held for the next step (LP <= 16 * 1024)
     uint64_t wpair = 0;       // wave 0: pairing draws of steps pbase .. pbase + 63, one per lane
     int32_t pbase = -kWave;
     for (int32_t pos = 0; pos < K; ++pos) {
@@ -1133,7 +1133,7 @@ extern "C" int routepack_pack_rows(const routepack_problem *prob, const int32_t 
             hipLaunchKernelGGL(k_pack_fit, dim3(nb), dim3(64), fit_lds, stream, ta, pf);
         }
         hipLaunchKernelGGL(k_pack_cellsum, dim3(K, nb), dim3(128), (size_t)4 * LP, stream, ta, pf);
-        hipLaunchKernelGGL(k_pack_pair, dim3(nb), dim3(256), (size_t)pair_lds, stream, ta, pf);
+        hipLaunchKernelGGL(k_pack_pair, dim3(nb), dim3(1024), (size_t)pair_lds, stream, ta, pf);
     } else {
         hipLaunchKernelGGL(k_pack_trials, dim3(nb), dim3(64), 0, stream, ta);
     }
