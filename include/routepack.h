@@ -266,7 +266,7 @@ int routepack_row_lower_bound(const routepack_problem *prob, const int32_t *leng
  *   layout       int32 [N] out or NULL: the cell of each sample in the
  *                first solution (written only when feasible)
  * Synchronizes.  A sample over capacity, or more cells than samples, is
- * infeasible (status 0, no node).  E_UNSUPPORTED when 8 (R D + N) bytes
+ * infeasible (status 0, no node).  E_UNSUPPORTED when 8 R D + 4 N bytes
  * exceed 150 KiB of LDS. */
 int routepack_fixed_bin_search(const routepack_problem *prob, const int32_t *lengths, int32_t n_rows,
                                int64_t node_budget, int32_t *status, int64_t *nodes, int32_t *layout,

@@ -15,7 +15,8 @@
 // feasible set X_R non-empty?) as a depth-first branch and bound under a
 // node budget, in a fixed order so that its verdict, node count and first
 // solution are defined:
-//   k_fixed_bin       one wave: samples in (-t, i) order go to an open cell
+//   k_fixed_bin       one wave, the cell loads and the choices in LDS, the
+//                     sorted lengths read from memory: samples in (-t, i) order go to an open cell
 //                     with room, lowest index first (a 64-lane ballot per
 //                     64 cells), then to the first unopened cell; a sample
 //                     equal in length to the previous one goes to no lower
@@ -65,6 +66,12 @@ __global__ void __launch_bounds__(1024) k_prefix(const int64_t *ts, int32_t N, i
     }
 }
 
+// ts[u] = t[sigma[u]] as int32: the lengths in (-t, i) order for the search.
+__global__ void k_sorted_lengths32(const int32_t *t, const int32_t *sigma, int32_t N, int32_t *ts) {
+    const int32_t u = blockIdx.x * blockDim.x + threadIdx.x;
+    if (u < N) ts[u] = t[sigma[u]];
+}
+
 // #{u : ts[u] > x} in the decreasing array ts.
 __device__ inline int32_t count_above(const int64_t *ts, int32_t N, int64_t x) {
     int32_t lo = 0, hi = N;  // ts[< lo] > x, ts[>= hi] <= x
@@ -106,18 +113,15 @@ __global__ void k_cell_bounds(const int64_t *ts, const int64_t *ps, int32_t N, i
     atomicMax(best, (unsigned long long)v);
 }
 
-__global__ void __launch_bounds__(kWave) k_fixed_bin(const int32_t *t, const int32_t *sigma, int32_t n, int64_t C,
-                                                     int32_t K, int64_t budget, int64_t *out, int32_t *cells) {
+__global__ void __launch_bounds__(kWave) k_fixed_bin(const int32_t *__restrict__ ts, int32_t n, int64_t C,
+                                                     int32_t K, int64_t budget, const int32_t *__restrict__ sigma,
+                                                     int64_t *out, int32_t *cells) {
     extern __shared__ __align__(16) char smem[];
     int64_t *load = reinterpret_cast<int64_t *>(smem);       // [K]
     int32_t *choice = reinterpret_cast<int32_t *>(load + K);  // [n] cell of sample h, -1 none
-    int32_t *ts = choice + n;                                 // [n] lengths in (-t, i) order
     const int lane = lane_id();
     for (int32_t c = lane; c < K; c += kWave) load[c] = 0;
-    for (int32_t u = lane; u < n; u += kWave) {
-        ts[u] = t[sigma[u]];
-        choice[u] = -1;
-    }
+    for (int32_t u = lane; u < n; u += kWave) choice[u] = -1;
     __syncthreads();
     int32_t h = 0, opened = 0;
     int64_t nodes = 0, status = 0;
@@ -236,18 +240,21 @@ extern "C" int routepack_fixed_bin_search(const routepack_problem *prob, const i
         return ROUTEPACK_OK;
     }
     const int32_t K = (int32_t)K64;
-    const size_t lds = 8 * (size_t)K + 8 * (size_t)N;
+    const size_t lds = 8 * (size_t)K + 4 * (size_t)N;
     if (lds > 150 * 1024) return ROUTEPACK_E_UNSUPPORTED;
     Scratch scr(stream);
     int32_t *sigma = scr.get<int32_t>(N);
+    int32_t *ts = scr.get<int32_t>(N);
     int64_t *out = scr.get<int64_t>(2);
     if (scr.failed()) return ROUTEPACK_E_DEVICE;
     RP_TRY(rank_sort_desc(lengths, N, sigma, stream));
+    hipLaunchKernelGGL(k_sorted_lengths32, dim3((N + 255) / 256), dim3(256), 0, stream, lengths,
+                       (const int32_t *)sigma, N, ts);
     if (hipFuncSetAttribute((const void *)k_fixed_bin, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
         hipSuccess)
         return ROUTEPACK_E_DEVICE;
-    hipLaunchKernelGGL(k_fixed_bin, dim3(1), dim3(kWave), lds, stream, lengths, (const int32_t *)sigma, N, C, K,
-                       node_budget, out, layout);
+    hipLaunchKernelGGL(k_fixed_bin, dim3(1), dim3(kWave), lds, stream, (const int32_t *)ts, N, C, K, node_budget,
+                       (const int32_t *)sigma, out, layout);
     RP_HIP(hipGetLastError());
     int64_t h[2] = {0, 0};
     RP_HIP(hipMemcpyAsync(h, out, sizeof(h), hipMemcpyDeviceToHost, stream));

@@ -626,10 +626,11 @@ def test_fixed_bin_search_matches_oracle(seed):
 
 
 @gpu
-@pytest.mark.parametrize("name", ["tiny", "small", "mid"])
+@pytest.mark.parametrize("name", ["tiny", "small", "mid", "heavy", "stress"])
 def test_fixed_bin_search_windows(name):
     """At the row bound of each window the search finds the oracle's layout
-    (over 64 cells on small and mid: the ballot runs over several chunks)."""
+    (over 64 cells from small on: the ballot runs over several chunks; 1984
+    cells and 32768 samples on stress)."""
     from oracle import bounds
     rp = _rp()
     w = synth.make_window(name)
@@ -663,9 +664,9 @@ def test_fixed_bin_search_edges():
     with pytest.raises(rp.RoutepackError) as ei:                       # a length below 1
         rp.fixed_bin_search(pb, t3, 5, 10)
     assert ei.value.code == -1
-    big = _search_problem(rp, 20000, 1, 100)
-    with pytest.raises(rp.RoutepackError) as ei:                       # 8 (K + N) bytes over 150 KiB
-        rp.fixed_bin_search(big, np.full(20000, 10, dtype=np.int32), 100, 10)
+    big = _search_problem(rp, 40000, 1, 100)
+    with pytest.raises(rp.RoutepackError) as ei:                       # 8 K + 4 N bytes over 150 KiB
+        rp.fixed_bin_search(big, np.full(40000, 10, dtype=np.int32), 100, 10)
     assert ei.value.code == -8
 
 
