@@ -2,7 +2,8 @@
 16 slots, cap 131072) and stress (32768 samples, 64 layers, 512 experts,
 64 ranks, 32 slots, cap 131072, 4 GiB of demand) windows at full size.
 
-Aggregation, placement, projection and packing are compared in full.
+Aggregation, placement, projection, packing and QualityDiversitySelect are
+compared in full.
 Annealing runs the full population for one level on the GPU; a sample of
 members is recomputed by the oracle under their own replica ids (every
 member's level is an independent chain given its start state)."""
@@ -68,3 +69,21 @@ def test_large_window_full_path(name):
     gt = ga["trace"].cpu().numpy()[0]
     assert np.array_equal(gt[ids], oa["trace"][0])
     assert np.array_equal(ga["population"].cpu().numpy()[ids], oa["population"])
+
+
+@gpu
+@pytest.mark.parametrize("name", ["heavy", "stress"])
+def test_large_window_select_population(name):
+    """QualityDiversitySelect over the window's distinct seeds at full size:
+    the order and the filled population equal the oracle's."""
+    from oracle import qds
+    import paper_2608_12146_amd as rp
+    w, pd, pb, agg, slot, load, q, pr = _prepared(name)
+    M = pr["n_distinct"]
+    cands, s0 = pr["population"][:M], pr["scores"][:M, 0]
+    _log(f"{name}: select_population over {M} candidates")
+    want = qds.select(pb, w.lengths, q, pr["r_star"], cands, s0, w.seed_pack)
+    got = rp.select_population(rp.Problem.from_dict(pd), w.lengths, q, pr["r_star"], cands, s0, w.seed_pack,
+                               pop_size=w.pop)
+    assert got["order"].cpu().tolist() == want.tolist()
+    assert np.array_equal(got["population"].cpu().numpy(), qds.population(cands, want, w.pop))
