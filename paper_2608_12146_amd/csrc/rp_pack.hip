@@ -364,7 +364,7 @@ __global__ void __launch_bounds__(64) k_pack_trials(TrialArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Seed trials in three launches for the common shapes (C < 2^32, N and K
+// Seed trials in three launches for the common shapes (C < 2^31, N and K
 // below 2^16, the trial's W table within LDS); the single-kernel path above
 // covers the rest.  Same draws, same decisions.
 //
@@ -655,12 +655,18 @@ __global__ void __launch_bounds__(64) k_pack_fit_reg(TrialArgs a, PackFast pf) {
                 }
                 c = 0xFFFF - (int32_t)(best & 0xFFFF);
             }
+            // c is uniform: only its chunk's owner lane changes
+            const int32_t cu = c >> 6;
+            const bool own = (c & (kWave - 1)) == lane;
 #pragma unroll
             for (int u = 0; u < NCH; ++u)
-                if (u * kWave + lane == c) {
-                    Tr[u] += ti;
-                    nr[u] += 1;
-                    kr[u] = fit_key(Tr[u], nr[u], c);
+                if (u == cu) {
+                    if (own) {
+                        Tr[u] += ti;
+                        nr[u] += 1;
+                        kr[u] = fit_key(Tr[u], nr[u], c);
+                    }
+                    break;
                 }
             if (lane == 0) cellk[item] = c;
         }
