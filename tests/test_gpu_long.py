@@ -6,8 +6,9 @@ and x* equal the oracle's.
   256, 1000 levels of 256 proposals, about 0.7 M evaluated moves), one and
   two attention stages: seconds;
 - mid (4096 samples, 24 layers, 256 experts, 16 ranks, 8 slots; population
-  1024, 2000 levels, about 43.5 M evaluated moves): minutes of oracle time,
-  so it runs only when ROUTEPACK_LONG_TESTS=1."""
+  1024, 2000 levels, about 43.5 M evaluated moves) with one or two EDP
+  shards or two stages: over a minute of oracle time each, so it runs only
+  when ROUTEPACK_LONG_TESTS=1."""
 import os
 
 import numpy as np
@@ -19,11 +20,11 @@ gpu = pytest.mark.gpu
 LONG = os.environ.get("ROUTEPACK_LONG_TESTS") == "1"
 
 
-def _full_schedule(name, S):
+def _full_schedule(name, S, G=1):
     import oracle as O
     import paper_2608_12146_amd as rp
     from synth import windows as W
-    w = synth.make_window(name)
+    w = synth.make_window(name, edp=G)
     pd = synth.window_problem(w, stages=S)
     pb = O.Problem.from_dict(pd)
     slot, _ = O.place(O.aggregate(w.demand), w.n_ranks)
@@ -31,12 +32,12 @@ def _full_schedule(name, S):
     pr = O.pack_rows(pb, w.lengths, q, w.seed_pack, W.N_TRIALS, W.CHOICE_WIDTH, w.pop)
     assert pr["rc"] == 0
     temps = synth.anneal_temperatures(w.levels)
-    print(f"[gpu-long] {name} S={S}: {w.levels} levels on the GPU", flush=True)
+    print(f"[gpu-long] {name} G={G} S={S}: {w.levels} levels on the GPU", flush=True)
     g = rp.anneal(rp.Problem.from_dict(pd), w.lengths, q, pr["r_star"], pr["population"], temps,
                   W.STEPS_PER_LEVEL, w.seed_anneal)
     assert g["level_kernel"] == "chain_run"
     threads = min(16, os.cpu_count() or 1)
-    print(f"[gpu-long] {name} S={S}: the oracle on {threads} threads", flush=True)
+    print(f"[gpu-long] {name} G={G} S={S}: the oracle on {threads} threads", flush=True)
     o = O.anneal(pb, w.lengths, q, pr["r_star"], pr["population"], temps, W.STEPS_PER_LEVEL, w.seed_anneal,
                  n_threads=threads)
     assert o["rc"] == 0
@@ -45,7 +46,7 @@ def _full_schedule(name, S):
     assert np.array_equal(g["population"].cpu().numpy(), o["population"])
     assert np.array_equal(g["best_layout"].cpu().numpy(), o["best_layout"])
     assert np.array_equal(g["best_score"].cpu().numpy(), o["best_score"])
-    print(f"[gpu-long] {name} S={S}: {int(o['trace'][:, :, 7].sum())} evaluated moves equal", flush=True)
+    print(f"[gpu-long] {name} G={G} S={S}: {int(o['trace'][:, :, 7].sum())} evaluated moves equal", flush=True)
 
 
 @gpu
@@ -56,5 +57,8 @@ def test_anneal_full_schedule_small(S):
 
 @gpu
 @pytest.mark.skipif(not LONG, reason="minutes of oracle time: set ROUTEPACK_LONG_TESTS=1")
-def test_anneal_full_schedule_mid():
-    _full_schedule("mid", 1)
+@pytest.mark.parametrize("G,S", [(1, 1), (2, 1), (1, 2)])
+def test_anneal_full_schedule_mid(G, S):
+    """The common shape, two EDP shards (100 row-shards: two per lane) and
+    two attention stages."""
+    _full_schedule("mid", S, G)
