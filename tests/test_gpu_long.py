@@ -1,6 +1,6 @@
-"""Full-schedule annealing parity on the default whole-schedule kernel:
-every level's trace, the parents of every resampling, the final population
-and x* equal the oracle's.
+"""Full-schedule annealing parity: every level's trace, the parents of every
+resampling, the final population and x* equal the oracle's (on the
+whole-schedule kernel where the window fits it).
 
 - small (1024 samples, 16 layers, 64 experts, 8 ranks, 4 slots; population
   256, 1000 levels of 256 proposals, about 0.7 M evaluated moves), one and
@@ -20,7 +20,7 @@ gpu = pytest.mark.gpu
 LONG = os.environ.get("ROUTEPACK_LONG_TESTS") == "1"
 
 
-def _full_schedule(name, S, G=1):
+def _full_schedule(name, S, G=1, chunk=250, kernel="chain_run", levels=None):
     import oracle as O
     import paper_2608_12146_amd as rp
     from synth import windows as W
@@ -31,28 +31,58 @@ def _full_schedule(name, S, G=1):
     q = O.project(w.demand, slot, w.n_ranks)
     pr = O.pack_rows(pb, w.lengths, q, w.seed_pack, W.N_TRIALS, W.CHOICE_WIDTH, w.pop)
     assert pr["rc"] == 0
-    temps = synth.anneal_temperatures(w.levels)
-    print(f"[gpu-long] {name} G={G} S={S}: {w.levels} levels on the GPU", flush=True)
+    all_temps = synth.anneal_temperatures(w.levels)
+    n = levels or w.levels  # the first n levels of the window's schedule
+    temps, t_after = all_temps[:n], (all_temps[n] if n < w.levels else 0.0)
+    print(f"[gpu-long] {name} G={G} S={S}: {n} levels on the GPU", flush=True)
     g = rp.anneal(rp.Problem.from_dict(pd), w.lengths, q, pr["r_star"], pr["population"], temps,
-                  W.STEPS_PER_LEVEL, w.seed_anneal)
-    assert g["level_kernel"] == "chain_run"
+                  W.STEPS_PER_LEVEL, w.seed_anneal, t_next=t_after)
+    print(f"[gpu-long] {name} G={G} S={S}: level kernel {g['level_kernel']}", flush=True)
+    if kernel:
+        assert g["level_kernel"] == kernel
     threads = min(16, os.cpu_count() or 1)
-    print(f"[gpu-long] {name} G={G} S={S}: the oracle on {threads} threads", flush=True)
-    o = O.anneal(pb, w.lengths, q, pr["r_star"], pr["population"], temps, W.STEPS_PER_LEVEL, w.seed_anneal,
-                 n_threads=threads)
-    assert o["rc"] == 0
-    assert np.array_equal(g["trace"].cpu().numpy(), o["trace"])
-    assert np.array_equal(g["parents"].cpu().numpy(), o["parents"])
-    assert np.array_equal(g["population"].cpu().numpy(), o["population"])
-    assert np.array_equal(g["best_layout"].cpu().numpy(), o["best_layout"])
-    assert np.array_equal(g["best_score"].cpu().numpy(), o["best_score"])
-    print(f"[gpu-long] {name} G={G} S={S}: {int(o['trace'][:, :, 7].sum())} evaluated moves equal", flush=True)
+    gt, gp = g["trace"].cpu().numpy(), g["parents"].cpu().numpy()
+    # The oracle in chunks of levels, each resuming from the last one's
+    # population and x* (a resumed run equals an uninterrupted one), so that
+    # every chunk is checked and reported as it ends.
+    pop, bl, bs, evals = pr["population"], None, None, 0
+    for lo in range(0, n, chunk):
+        hi = min(n, lo + chunk)
+        o = O.anneal(pb, w.lengths, q, pr["r_star"], pop, temps[lo:hi], W.STEPS_PER_LEVEL, w.seed_anneal,
+                     t_next=temps[hi] if hi < n else t_after, sweep_offset=lo, best_layout=bl, best_score=bs,
+                     n_threads=threads)
+        assert o["rc"] == 0
+        assert np.array_equal(gt[lo:hi], o["trace"]), (lo, hi)
+        assert np.array_equal(gp[lo:hi], o["parents"]), (lo, hi)
+        pop, bl, bs = o["population"], o["best_layout"], o["best_score"]
+        evals += int(o["trace"][:, :, 7].sum())
+        print(f"[gpu-long] {name} G={G} S={S}: levels {lo}-{hi - 1} equal on {threads} threads", flush=True)
+    assert np.array_equal(g["population"].cpu().numpy(), pop)
+    assert np.array_equal(g["best_layout"].cpu().numpy(), bl)
+    assert np.array_equal(g["best_score"].cpu().numpy(), bs)
+    print(f"[gpu-long] {name} G={G} S={S}: {evals} evaluated moves equal", flush=True)
 
 
 @gpu
 @pytest.mark.parametrize("S", [1, 2])
 def test_anneal_full_schedule_small(S):
     _full_schedule("small", S)
+
+
+@gpu
+@pytest.mark.skipif(not LONG, reason="minutes of oracle time: set ROUTEPACK_LONG_TESTS=1")
+@pytest.mark.parametrize("name", ["heavy", "stress"])
+def test_anneal_full_schedule_large(name):
+    """The first 1000 of the heavy-tail window's 2000 levels (population
+    2048; about ten minutes of oracle time, reported every 50 levels) and the
+    first 10 of the stress window's 500 (population 4096; the oracle needs
+    seconds to minutes per level there, reported every level), on whichever
+    level kernel the library picks (more than 32 layers rule out the chain
+    kernels)."""
+    if name == "heavy":
+        _full_schedule(name, 1, chunk=50, kernel=None, levels=1000)
+    else:
+        _full_schedule(name, 1, chunk=1, kernel=None, levels=10)
 
 
 @gpu
