@@ -74,15 +74,15 @@ def test_anneal_full_schedule_small(S):
 @pytest.mark.parametrize("name", ["heavy", "stress"])
 def test_anneal_full_schedule_large(name):
     """The first 1000 of the heavy-tail window's 2000 levels (population
-    2048; about ten minutes of oracle time, reported every 50 levels) and the
-    first 10 of the stress window's 500 (population 4096; the oracle needs
-    seconds to minutes per level there, reported every level), on whichever
-    level kernel the library picks (more than 32 layers rule out the chain
-    kernels)."""
+    2048; about eleven minutes of oracle time, reported every 50 levels) and
+    the first 4 of the stress window's 500 (population 4096; about two and a
+    half minutes of oracle time per level, reported every level), on
+    whichever level kernel the library picks (more than 32 layers rule out
+    the chain kernels)."""
     if name == "heavy":
         _full_schedule(name, 1, chunk=50, kernel=None, levels=1000)
     else:
-        _full_schedule(name, 1, chunk=1, kernel=None, levels=10)
+        _full_schedule(name, 1, chunk=1, kernel=None, levels=4)
 
 
 @gpu
