@@ -79,7 +79,10 @@ typedef struct routepack_problem {
  * exact in int64.
  *   demand  int32 [N][L][E]   replayed routing counts, >= 0
  *   agg     int64 [L][E]      out
- * Asynchronous.  E_INVALID on null pointers or negative sizes. */
+ * Asynchronous; allocates stream-ordered scratch of one int64 per column of
+ * L E and band of at least 64 rows (at most 4096 / ceil(L E / 256) + 1 bands).
+ * E_INVALID on null pointers or negative sizes; E_DEVICE when the scratch
+ * cannot be allocated. */
 int routepack_aggregate_demand(const routepack_problem *prob, const int32_t *demand,
                                int64_t *agg, hipStream_t stream);
 
