@@ -40,7 +40,7 @@ constexpr int kMaxCells = 4096;
 
 __global__ void __launch_bounds__(256) k_rank_sort(const int32_t *__restrict__ t, int32_t N,
                                                    int32_t *__restrict__ sigma) {
-    __shared__ int32_t tile[1024];
+    __shared__ __align__(16) int32_t tile[1024];
     const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
     const int32_t ti = i < N ? t[i] : 0;
     int32_t rank = 0;
@@ -48,7 +48,19 @@ __global__ void __launch_bounds__(256) k_rank_sort(const int32_t *__restrict__ t
         for (int x = threadIdx.x; x < 1024; x += blockDim.x) tile[x] = base + x < N ? t[base + x] : -1;
         __syncthreads();
         const int32_t lim = N - base < 1024 ? N - base : 1024;
-        for (int x = 0; x < lim; ++x) {
+        // four lengths per 16-byte LDS read, several reads in flight
+        const int4 *t4 = reinterpret_cast<const int4 *>(tile);
+        const int32_t lim4 = lim >> 2;
+#pragma unroll 4
+        for (int x4 = 0; x4 < lim4; ++x4) {
+            const int4 v = t4[x4];
+            const int32_t x = base + 4 * x4;
+            rank += (v.x > ti) || (v.x == ti && x < i);
+            rank += (v.y > ti) || (v.y == ti && x + 1 < i);
+            rank += (v.z > ti) || (v.z == ti && x + 2 < i);
+            rank += (v.w > ti) || (v.w == ti && x + 3 < i);
+        }
+        for (int x = 4 * lim4; x < lim; ++x) {
             const int32_t tj = tile[x];
             rank += (tj > ti) || (tj == ti && base + x < i);
         }
