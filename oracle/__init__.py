@@ -204,6 +204,51 @@ def pack_rows(prob: Problem, lengths, q, seed, n_trials, width, pop):
                 scores=sc, r_lb=int(extra[0]), n_distinct=int(extra[1]), n_trials_ok=int(extra[2]))
 
 
+def seed_trial(prob: Problem, lengths, q, n_rows, width, seed, trial):
+    """One randomized seed trial of Alg. 2 with its steps exposed (Sec. 4.1.1):
+    dict(ok, pi = the WindowShuffle order, cellk = the RandomizedBestFit cell
+    k in [0, R*D) of each sample, layout = the cell id r*D + d after
+    EDPAwarePair)."""
+    lib = _load()
+    t = np.ascontiguousarray(lengths, dtype=np.int32)
+    qq = np.ascontiguousarray(q, dtype=np.int32)
+    N = prob.n_samples
+    pi = np.full(N, -1, dtype=np.int32)
+    ck = np.full(N, -1, dtype=np.int32)
+    lay = np.full(N, -1, dtype=np.int32)
+    rc = lib.or_seed_trial(prob.ref, _p(t, C.c_int32), _p(qq, C.c_int32), C.c_int32(n_rows),
+                           C.c_int32(width), C.c_uint64(seed), C.c_uint64(trial),
+                           _p(pi, C.c_int32), _p(ck, C.c_int32), _p(lay, C.c_int32))
+    if rc < 0:
+        raise ValueError(f"or_seed_trial rc={rc}")
+    return dict(ok=bool(rc), pi=pi, cellk=ck, layout=lay)
+
+
+def edp_pair(prob: Problem, q, n_rows, cellk, width, seed, trial):
+    """EDPAwarePair alone (Sec. 4.1.1) on completed cells cellk[i] in
+    [0, R*D): returns the layout (cell id r*D + d per sample)."""
+    lib = _load()
+    qq = np.ascontiguousarray(q, dtype=np.int32)
+    ck = np.ascontiguousarray(cellk, dtype=np.int32)
+    lay = np.full(prob.n_samples, -1, dtype=np.int32)
+    rc = lib.or_edp_pair(prob.ref, _p(qq, C.c_int32), C.c_int32(n_rows), _p(ck, C.c_int32),
+                         C.c_int32(width), C.c_uint64(seed), C.c_uint64(trial), _p(lay, C.c_int32))
+    if rc:
+        raise ValueError(f"or_edp_pair rc={rc}")
+    return lay
+
+
+def energy(prob: Problem, scores):
+    """Eq. pa-energy of score triples [n][3]: (S0 + 1e-6 S1) + 1e-9 S2 with
+    S_i = s_i / (2^F C)."""
+    lib = _load()
+    s = np.ascontiguousarray(np.asarray(scores, dtype=np.int64).reshape(-1, 3))
+    out = np.zeros(len(s), dtype=np.float64)
+    lib.or_energy(C.c_int32(len(s)), _p(s, C.c_int64), C.c_int32(prob.frac_bits),
+                  C.c_int64(prob.capacity), _p(out, C.c_double))
+    return out
+
+
 def resample(energies, t_cur, t_next, seed, level):
     """Systematic resampling of one level boundary -> parent indices [pop]."""
     lib = _load()
@@ -211,6 +256,17 @@ def resample(energies, t_cur, t_next, seed, level):
     par = np.zeros(len(e), dtype=np.int32)
     lib.or_resample(C.c_int32(len(e)), _p(e, C.c_double), C.c_double(t_cur), C.c_double(t_next),
                     C.c_uint64(seed), C.c_int32(level), _p(par, C.c_int32))
+    return par
+
+
+def resample_at(energies, t_cur, t_next, V):
+    """The systematic resampling step for a given uniform V in [0, 2^32)
+    (u_0 = V / (2^32 P)) -> parent indices [pop]."""
+    lib = _load()
+    e = np.ascontiguousarray(energies, dtype=np.float64)
+    par = np.zeros(len(e), dtype=np.int32)
+    lib.or_resample_at(C.c_int32(len(e)), _p(e, C.c_double), C.c_double(t_cur), C.c_double(t_next),
+                       C.c_uint64(V), _p(par, C.c_int32))
     return par
 
 

@@ -22,6 +22,18 @@ import numpy as np
 def score_exact(prob, lengths, q, R, layout):
     """Normalised score tuple (max_g U_g, sum_g U_g, max_{r,g} J) as Fractions,
     or None when the layout is infeasible."""
+    J = row_shard_costs_exact(prob, lengths, q, R, layout)
+    if J is None:
+        return None
+    G = prob.n_edp
+    U = [sum(J[(r, g)] for r in range(R)) for g in range(G)]
+    return (max(U), sum(U), max(J.values()))
+
+
+def row_shard_costs_exact(prob, lengths, q, R, layout):
+    """J_{r,g} = A_{r,g} + E_{r,g} (Eqs. stage-aware-attention, row-expert-load,
+    row-expert-cost) as Fractions keyed by (r, g), or None when the layout is
+    infeasible."""
     D, G, C = prob.n_dp, prob.n_edp, prob.capacity
     L, P = prob.n_layers, prob.n_ranks
     t = [int(x) for x in lengths]
@@ -55,8 +67,7 @@ def score_exact(prob, lengths, q, R, layout):
                      for p in range(P)]
                 E += Fraction(max(W), C)
             J[(r, g)] = A + E
-    U = [sum(J[(r, g)] for r in range(R)) for g in range(G)]
-    return (max(U), sum(U), max(J.values()))
+    return J
 
 
 def fixed_point_to_fraction(s, prob):

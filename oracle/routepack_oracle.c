@@ -7,7 +7,8 @@
  * baseline leg of the benchmark load it.  It shares no header, helper or
  * constant table with the HIP sources.
  *
- * Coverage and pins (see tests/test_oracle_*.py):
+ * Coverage and pins (tests/test_oracle_pins.py and
+ * tests/test_oracle_operator_pins.py):
  *   or_philox4x64      Philox4x64-10 (Salmon et al., SC'11) -- pinned to
  *                      numpy.random.Philox.
  *   or_exp_det         exp(x) for x <= 0 by Cody-Waite reduction and a
@@ -21,15 +22,31 @@
  *                      pinned to a one-hot einsum and the top-k invariant.
  *   or_score           Eqs. cell-token-statistics .. lexicographic-score in
  *                      fixed point -- pinned to exact rational brute force.
- *   or_diag            online load diagnostics (Eqs. global-ep-cv,
- *                      ep-efficiency) -- pinned to float64 numpy formulas.
+ *                      Its load diagnostics (Sec. 5.3, Eqs. global-ep-cv and
+ *                      ep-efficiency) are pinned to the Fig. 3 numbers and to
+ *                      numpy on random loads.
  *   or_pack_rows       R* search, FixedRowFFD and Alg. 2 seeding -- pinned by
- *                      invariants and exhaustive minimum row counts.
+ *                      invariants and exhaustive minimum row counts; its
+ *                      operators (WindowShuffle, RandomizedBestFit,
+ *                      EDPAwarePair; exported one at a time as or_seed_trial
+ *                      and or_edp_pair) by hand-traced instances and by the
+ *                      bounded draws of numpy's Philox.
  *   or_anneal          Alg. 3 population annealing -- incremental score pinned
- *                      to full rescoring at every step; the trajectory itself
- *                      is parity unpinned by the paper (special cases only:
+ *                      to full rescoring at every step; GuidedProposal's
+ *                      three roulettes and the random branch by one-step
+ *                      proposals predicted from numpy's Philox and exact
+ *                      row-shard costs; Eq. pa-energy and the normalised
+ *                      Delta by accept thresholds at a known u; the strict
+ *                      tie rules of the trajectory best and the incumbent by
+ *                      equal-score twins.  The trajectory as a whole is
+ *                      parity unpinned by the paper (special cases only:
  *                      all-tie acceptance, greedy limit, non-regression,
  *                      exhaustive optimum as a lower bound).
+ *   or_resample(_at)   systematic resampling -- pinned by offspring counts,
+ *                      the literal F_j >= u_m boundary at u_0 = 0, and exact
+ *                      systematic resampling on real weights.  The 2^40 scale
+ *                      at which weights are quantised is a determinism
+ *                      constant, not a quantity of the paper: parity unpinned.
  *
  * Fixed-point convention: every cost is an int64 in units of 2^-F raw tokens,
  * so a normalised cost of the paper (divided by C) is value / (2^F * C).
@@ -632,7 +649,7 @@ static int cmp_fit(const void *a, const void *b)
  * rest, then EDPAwarePair.  Returns 1 and fills layout on success. */
 static int seed_trial(const or_problem *pb, const topo_t *tp, const int32_t *t, const int32_t *q,
                       int32_t R, const int32_t *sigma, int32_t w, uint64_t seed, uint64_t trial,
-                      int32_t *layout)
+                      int32_t *layout, int32_t *pi_out, int32_t *cellk_out)
 {
     int32_t N = pb->n_samples;
     int64_t K = (int64_t)R * pb->n_dp, C = pb->capacity;
@@ -665,6 +682,8 @@ static int seed_trial(const or_problem *pb, const topo_t *tp, const int32_t *t, 
         int32_t c = feas[rho].c;
         cellk[i] = c; T[c] += t[i]; cnt[c] += 1;
     }
+    if (pi_out) memcpy(pi_out, pi, sizeof(int32_t) * N);
+    if (ok && cellk_out) memcpy(cellk_out, cellk, sizeof(int32_t) * N);
     if (ok) edp_aware_pair(pb, tp, q, R, cellk, w, seed, trial, layout);
     free(remaining); free(pi); free(cellk); free(T); free(cnt); free(feas);
     return ok;
@@ -747,7 +766,7 @@ int or_pack_rows(const or_problem *pb, const int32_t *t, const int32_t *q, uint6
             memcpy(tmp, lex_lt(s_pair, s_len) ? paired : x_len, sizeof(int32_t) * N);
             free(paired);
         } else {
-            ok = seed_trial(pb, &tp, t, q, (int32_t)R, sigma, w, seed, (uint64_t)(m - 1), tmp);
+            ok = seed_trial(pb, &tp, t, q, (int32_t)R, sigma, w, seed, (uint64_t)(m - 1), tmp, NULL, NULL);
             if (ok) {
                 int64_t s[3];
                 if (or_score(pb, t, q, (int32_t)R, tmp, s, NULL, NULL, NULL) != 0) ok = 0;
@@ -777,6 +796,45 @@ int or_pack_rows(const or_problem *pb, const int32_t *t, const int32_t *q, uint6
     return OR_OK;
 }
 
+/* The seeding operators one at a time, so that each can be checked on its
+ * own (Sec. 4.1.1).  or_seed_trial runs one randomized trial with R rows:
+ * pi_out receives the WindowShuffle order, cellk_out the cell k in [0, R*D)
+ * each sample's RandomizedBestFit gave it, layout_out the cell id r*D + d
+ * after EDPAwarePair; returns 1, or 0 when best-fit found no feasible cell
+ * (then cellk_out and layout_out are untouched).  or_edp_pair runs
+ * EDPAwarePair alone on given completed cells. */
+int or_seed_trial(const or_problem *pb, const int32_t *t, const int32_t *q, int32_t R, int32_t w,
+                  uint64_t seed, uint64_t trial, int32_t *pi_out, int32_t *cellk_out,
+                  int32_t *layout_out)
+{
+    if (check_problem(pb) || R < 1 || w < 1) return OR_INVALID;
+    int32_t N = pb->n_samples;
+    if ((int64_t)R * pb->n_dp > N) return OR_INVALID;
+    int32_t *sigma = malloc(sizeof(int32_t) * N);
+    for (int32_t i = 0; i < N; ++i) sigma[i] = i;
+    g_len = t;
+    qsort(sigma, N, sizeof(int32_t), cmp_len_desc);
+    topo_t tp;
+    topo_build(pb, &tp);
+    int ok = seed_trial(pb, &tp, t, q, R, sigma, w, seed, trial, layout_out, pi_out, cellk_out);
+    topo_free(&tp);
+    free(sigma);
+    return ok;
+}
+
+int or_edp_pair(const or_problem *pb, const int32_t *q, int32_t R, const int32_t *cellk, int32_t w,
+                uint64_t seed, uint64_t trial, int32_t *layout_out)
+{
+    if (check_problem(pb) || R < 1 || w < 1) return OR_INVALID;
+    int64_t K = (int64_t)R * pb->n_dp;
+    for (int32_t i = 0; i < pb->n_samples; ++i) if (cellk[i] < 0 || cellk[i] >= K) return OR_INVALID;
+    topo_t tp;
+    topo_build(pb, &tp);
+    edp_aware_pair(pb, &tp, q, R, cellk, w, seed, trial, layout_out);
+    topo_free(&tp);
+    return OR_OK;
+}
+
 /* ------------------------------------------------------------------------ */
 /* Population annealing (Alg. 3). */
 
@@ -796,6 +854,13 @@ static double energy_of(const int64_t *s, double scale)
     double S0 = (double)s[0] / scale, S1 = (double)s[1] / scale, S2 = (double)s[2] / scale;
     double e = S0 + 1e-6 * S1;
     return e + 1e-9 * S2;
+}
+
+/* Exported for the tests: the energy of n score triples. */
+void or_energy(int32_t n, const int64_t *s, int32_t frac_bits, int64_t capacity, double *out)
+{
+    double scale = (double)((int64_t)1 << frac_bits) * (double)capacity;
+    for (int32_t j = 0; j < n; ++j) out[j] = energy_of(s + (int64_t)j * 3, scale);
 }
 
 /* One replica's chain state. */
@@ -1114,8 +1179,20 @@ static void *worker(void *p)
  * quantised weights: w_j = floor(2^40 exp(-(1/T_next - 1/T_cur) E~_j)) with
  * E~_j = (E_j - E_min) / max(|E_min|, 1); F = inclusive prefix; with u0 drawn
  * as V / (2^32 P), member m takes parent min{ j : F_j / F_{P-1} >= u0 + m/P }. */
+void or_resample_at(int32_t pop, const double *energies, double t_cur, double t_next,
+                    uint64_t V, int32_t *parent);
+
 void or_resample(int32_t pop, const double *energies, double t_cur, double t_next,
                  uint64_t seed, int32_t level, int32_t *parent)
+{
+    uint64_t ctr[4] = {0, (uint64_t)(uint32_t)level, 0xFFFFFFFFull, 2}, key[2] = {seed, 0}, out[4];
+    or_philox4x64(ctr, key, out);
+    or_resample_at(pop, energies, t_cur, t_next, out[0] >> 32, parent);
+}
+
+/* The same step for a given V in [0, 2^32) (u0 = V / (2^32 P)). */
+void or_resample_at(int32_t pop, const double *energies, double t_cur, double t_next,
+                    uint64_t V, int32_t *parent)
 {
     double emin = energies[0];
     for (int32_t j = 1; j < pop; ++j) if (energies[j] < emin) emin = energies[j];
@@ -1131,9 +1208,6 @@ void or_resample(int32_t pop, const double *energies, double t_cur, double t_nex
         F[j] = acc;
     }
     uint64_t S = F[pop - 1];
-    uint64_t ctr[4] = {0, (uint64_t)(uint32_t)level, 0xFFFFFFFFull, 2}, key[2] = {seed, 0}, out[4];
-    or_philox4x64(ctr, key, out);
-    uint64_t V = out[0] >> 32;
     for (int32_t m = 0; m < pop; ++m) {
         unsigned __int128 rhs = (unsigned __int128)S * (V + ((uint64_t)m << 32));
         int32_t j = 0;
