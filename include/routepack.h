@@ -173,7 +173,8 @@ typedef struct routepack_anneal_params {
  *              P in {4, 8, 16}, L <= 32, R G <= 64, <= 16 slots per shard
  *   WAVE       one wave per member, lanes over flat 64-entry strides:
  *              R G <= 512, member state within LDS
- *   WORKGROUP  one workgroup per member, state in HBM: every valid problem */
+ *   WORKGROUP  one workgroup per member, state in HBM: every problem within
+ *              the limits that routepack_anneal states */
 #define ROUTEPACK_KERNEL_WORKGROUP 0
 #define ROUTEPACK_KERNEL_WAVE 1
 #define ROUTEPACK_KERNEL_CHAIN 2
@@ -205,10 +206,16 @@ typedef struct routepack_anneal_params {
  *                after the level, -1 when no resampling followed it
  *   step_log     uint8 [n_sweeps][pop_size][K] out or NULL: 0 infeasible,
  *                1 rejected, 2 accepted
- * Synchronizes.  E_LAYOUT when a population member (or the given x*) is not
- * feasible for R or best_score does not match x*; E_INTERNAL when the final
- * validation or the non-regression check fails; E_UNSUPPORTED when P is not
- * a power of two <= 64, L*P > 4096, or R*G > 4096. */
+ * Synchronizes.  E_DEVICE on a HIP error, and when a grid barrier or a
+ * hand-over wait of the whole-schedule kernel gives up: each wait polls a
+ * shared error flag and gives up after 2^22 polls (ROUTEPACK_WAIT_SPINS in
+ * the environment sets another bound, at least 32); every wave then leaves
+ * the kernel and the outputs are undefined.  E_LAYOUT when a population
+ * member (or the given x*) is not feasible for R or best_score does not
+ * match x*; E_INTERNAL when the final
+ * validation or the non-regression check fails; E_UNSUPPORTED (before any
+ * device work) when P is not a power of two <= 64, L*P > 4096, R*G > 512,
+ * G > 64, a shard holds more than 64 DP slots, or S > 4. */
 int routepack_anneal(const routepack_problem *prob, const int32_t *lengths, const int32_t *q,
                      int32_t n_rows, int32_t pop_size, int32_t *population,
                      const routepack_anneal_params *params, int32_t *best_layout,
@@ -217,7 +224,7 @@ int routepack_anneal(const routepack_problem *prob, const int32_t *lengths, cons
 
 /* Exact objective of many layouts (Eqs. cell-token-statistics ..
  * lexicographic-score) with validation and the online load diagnostics of
- * Sec. 6.3 (Eqs. global-ep-cv and ep-efficiency).
+ * Sec. 5.3 (Eqs. global-ep-cv and ep-efficiency).
  *   layouts    int32 [n_layouts][N]
  *   scores     int64 [n_layouts][3]  out (INT64_MAX x3 for an invalid layout)
  *   status     int32 [n_layouts]     out: 0, or bit 0 a cell id outside [0, R*D),

@@ -85,6 +85,7 @@ struct RunArgs {
     int64_t blob_bytes;
     unsigned *pub;         // [pop] per slab: the last level whose image it published (zero at launch)
     unsigned *got;         // [pop] per slab: receivers that have copied its image (zero at launch)
+    unsigned spin_limit;   // polls before a barrier or hand-over wait gives up (sets err)
 };
 
 // Bytes of the whole-schedule kernel's level-end tables for a population.

@@ -906,8 +906,13 @@ __global__ void __launch_bounds__(1024) k_level_end(LevelEndArgs a) {
 }
 
 // population[m] = cell_of of slab parent[m] (or m).
+// Population rows from the slabs (member m from slab parent[m]).  With
+// err set (a wait of the whole-schedule kernel gave up, so the slab map may
+// be unwritten) it copies nothing.
 __global__ void k_gather_population(const char *slabs, int64_t slab_bytes, int64_t off_cell,
-                                    const int32_t *parent, int32_t N, int32_t *population) {
+                                    const int32_t *parent, int32_t N, int32_t *population,
+                                    const int32_t *err) {
+    if (err && *err) return;
     const int m = blockIdx.x;
     const int par = parent ? parent[m] : m;
     const int32_t *src = reinterpret_cast<const int32_t *>(slabs + (int64_t)par * slab_bytes + off_cell);
@@ -919,6 +924,15 @@ __global__ void k_compare_score(const int64_t *a, const int64_t *b, const int32_
 }
 
 static int64_t align_up(int64_t x) { return (x + 255) & ~(int64_t)255; }
+
+// Polls before a wait of the whole-schedule kernel gives up: 2^22 (seconds
+// of waiting), or ROUTEPACK_WAIT_SPINS (at least 32) when that is set.
+static unsigned wait_spin_limit() {
+    const char *v = getenv("ROUTEPACK_WAIT_SPINS");
+    if (!v || !*v) return 1u << 22;
+    const unsigned long x = strtoul(v, nullptr, 10);
+    return x < 32 ? 32u : (x > (1ul << 30) ? (1u << 30) : (unsigned)x);
+}
 
 static SlabOffsets slab_layout(int64_t N, int64_t B, int64_t RG, int64_t LP) {
     SlabOffsets o;
@@ -1209,6 +1223,7 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
         run.blob_bytes = blob_bytes;
         run.pub = flags;
         run.got = flags + pop_size;
+        run.spin_limit = wait_spin_limit();
         if (a.rv == 2) {  // the two-per-lane variant keeps its level-end tables in HBM
             run.lend_stride = run_lend_bytes(pop_size);
             run.lend = scr.get<char>((size_t)((pop_size + a.mpw - 1) / a.mpw) * (size_t)run.lend_stride);
@@ -1228,7 +1243,7 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
         }
         if (e1) RP_HIP(hipEventRecord(e1, stream));
         hipLaunchKernelGGL(k_gather_population, dim3(pop_size), dim3(256), 0, stream, slabA, off.bytes, off.cell,
-                           slab_final, N, population);
+                           slab_final, N, population, (const int32_t *)run.err);
         RP_HIP(hipGetLastError());
         RP_TRY(eval_layouts(prob, topo, dp, lengths, q, n_rows, 1, best_layout, chk_score, status, nullptr,
                             nullptr, nullptr, stream));
@@ -1301,10 +1316,10 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
     if (prm->n_sweeps > 0) {
         if (fast)
             hipLaunchKernelGGL(k_gather_population, dim3(pop_size), dim3(256), 0, stream, slabA, off.bytes,
-                               off.cell, slab_of[cur], N, population);
+                               off.cell, slab_of[cur], N, population, (const int32_t *)nullptr);
         else
             hipLaunchKernelGGL(k_gather_population, dim3(pop_size), dim3(256), 0, stream, src, off.bytes,
-                               off.cell, cur_parent, N, population);
+                               off.cell, cur_parent, N, population, (const int32_t *)nullptr);
     }
     RP_HIP(hipGetLastError());
     // Validate x* and the non-regression guarantee.

@@ -1117,8 +1117,6 @@ __global__ void __launch_bounds__(512) k_anneal_chain(AnnealArgs a) {
 
 namespace {
 
-constexpr unsigned kSpinLimit = 1u << 22;
-
 // Hand-over of a member to another wave through global memory: the raw LDS
 // region (16-byte units, all reads then all writes per batch) and the
 // registers.  Every lane of the wave takes part.
@@ -1216,7 +1214,7 @@ __device__ inline void member_receive(const AnnealArgs &a, char *mine, const cha
 
 // Grid-wide barrier on a monotonic arrival counter; false if it timed out
 // (then every workgroup stops).  Every thread of the workgroup takes part.
-__device__ inline bool grid_sync(unsigned *bar, unsigned target, int32_t *err, int32_t *s_ok) {
+__device__ inline bool grid_sync(unsigned *bar, unsigned target, int32_t *err, unsigned spin_limit, int32_t *s_ok) {
     __syncthreads();
     if (threadIdx.x == 0) {
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
@@ -1227,7 +1225,7 @@ __device__ inline bool grid_sync(unsigned *bar, unsigned target, int32_t *err, i
             __builtin_amdgcn_s_sleep(2);
             // (the error flag is polled every 32 spins: one load per spin)
             if ((++spins & 31) == 0 &&
-                (spins > kSpinLimit || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))) {
+                (spins > spin_limit || __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))) {
                 __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 good = 0;
                 break;
@@ -1242,7 +1240,7 @@ __device__ inline bool grid_sync(unsigned *bar, unsigned target, int32_t *err, i
 
 // Waits (one wave) until *p >= target, then acquires; false if it timed
 // out or another wait or barrier failed (the error flag is set).
-__device__ inline bool wave_wait_geq(const unsigned *p, unsigned target, int32_t *err) {
+__device__ inline bool wave_wait_geq(const unsigned *p, unsigned target, int32_t *err, unsigned spin_limit) {
     unsigned spins = 0;
     for (;;) {
         unsigned v = 0;
@@ -1252,7 +1250,7 @@ __device__ inline bool wave_wait_geq(const unsigned *p, unsigned target, int32_t
         if ((++spins & 31) == 0) {
             int32_t e = 0;
             if (lane_id() == 0) e = __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if (spins > kSpinLimit || __builtin_amdgcn_readlane(e, 0)) {
+            if (spins > spin_limit || __builtin_amdgcn_readlane(e, 0)) {
                 if (lane_id() == 0) __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 return false;
             }
@@ -1417,7 +1415,7 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
             for (int f = 0; f < 4; ++f) r.wg_best[((int64_t)(n & 1) * nb + blockIdx.x) * 4 + f] = s_k[0][f];
             r.wg_emin[(n & 1) * nb + blockIdx.x] = s_dred[0];
         }
-        if (!grid_sync(r.bar, (unsigned)nb * ++epoch, r.err, &s_ok)) return;  // A
+        if (!grid_sync(r.bar, (unsigned)nb * ++epoch, r.err, r.spin_limit, &s_ok)) return;  // A
 
         // ---- every workgroup: incumbent and minimum energy from the workgroup summaries
         const double t_next = n + 1 < r.n_sweeps ? r.temps[n + 1] : r.t_after;
@@ -1601,12 +1599,12 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
                 }
             }
         }
-        if (sync_b && !grid_sync(r.bar, (unsigned)nb * ++epoch, r.err, &s_ok)) return;  // B
+        if (sync_b && !grid_sync(r.bar, (unsigned)nb * ++epoch, r.err, r.spin_limit, &s_ok)) return;  // B
         if (resample) {
             for (int32_t mm = tid; mm < pop; mm += nt) slab[mm] = slabn[mm];
             __syncthreads();
             char *mine = smem + a.lds_shared + (int64_t)wv * a.lds_member;
-            if (active && src_slab >= 0 && (sync_b || wave_wait_geq(r.pub + src_slab, token, r.err))) {
+            if (active && src_slab >= 0 && (sync_b || wave_wait_geq(r.pub + src_slab, token, r.err, r.spin_limit))) {
                 member_receive<GV == 2 ? 2 : 1>(a, mine, r.blobs + (int64_t)src_slab * r.blob_bytes, R);
                 if (!sync_b) {
                     wave_copy16(a.slabs + (int64_t)src_slab * a.off.bytes + a.off.W,
@@ -1615,8 +1613,18 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
                     if (lane == 0) __hip_atomic_fetch_add(r.got + src_slab, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 }
             }
-            if (!sync_b && publish && wave_wait_geq(r.got + gw, (unsigned)n_recv, r.err) && lane == 0)
+            if (!sync_b && publish && wave_wait_geq(r.got + gw, (unsigned)n_recv, r.err, r.spin_limit) && lane == 0)
                 __hip_atomic_store(r.got + gw, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (!sync_b) {
+                // A wait that gave up has set the error flag: the whole
+                // workgroup leaves before a wave starts the next level on a
+                // state that was not received, or writes W rows that a
+                // receiver may still be copying.
+                __syncthreads();
+                if (tid == 0) s_ok = __hip_atomic_load(r.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0;
+                __syncthreads();
+                if (!s_ok) return;
+            }
         }
         m = m_next;
     }

@@ -6,9 +6,11 @@ whole-schedule kernel where the window fits it).
   256, 1000 levels of 256 proposals, about 0.7 M evaluated moves), one and
   two attention stages: seconds;
 - mid (4096 samples, 24 layers, 256 experts, 16 ranks, 8 slots; population
-  1024, 2000 levels, about 43.5 M evaluated moves) with one or two EDP
-  shards or two stages: over a minute of oracle time each, so it runs only
-  when ROUTEPACK_LONG_TESTS=1."""
+  1024, 2000 levels, about 43.5 M evaluated moves) with one EDP shard and one
+  stage, two EDP shards, and two stages: about a minute and a quarter of
+  oracle time each on 16 host threads;
+- the first 1000 levels of heavy and the first 4 of stress: minutes of
+  oracle time, so they run only when ROUTEPACK_LONG_TESTS=1."""
 import os
 
 import numpy as np
@@ -40,7 +42,7 @@ def _full_schedule(name, S, G=1, chunk=250, kernel="chain_run", levels=None):
     print(f"[gpu-long] {name} G={G} S={S}: level kernel {g['level_kernel']}", flush=True)
     if kernel:
         assert g["level_kernel"] == kernel
-    threads = min(16, os.cpu_count() or 1)
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
     gt, gp = g["trace"].cpu().numpy(), g["parents"].cpu().numpy()
     # The oracle in chunks of levels, each resuming from the last one's
     # population and x* (a resumed run equals an uninterrupted one), so that
@@ -86,7 +88,6 @@ def test_anneal_full_schedule_large(name):
 
 
 @gpu
-@pytest.mark.skipif(not LONG, reason="minutes of oracle time: set ROUTEPACK_LONG_TESTS=1")
 @pytest.mark.parametrize("G,S", [(1, 1), (2, 1), (1, 2)])
 def test_anneal_full_schedule_mid(G, S):
     """The common shape, two EDP shards (100 row-shards: two per lane) and

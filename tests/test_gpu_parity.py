@@ -99,9 +99,9 @@ def test_eval_objective(name, G, S):
     pr = _packed(name, G, S)
     R = pr["r_star"]
     lays = pr["population"][: min(w.pop, 32)].copy()
-    # add infeasible layouts: an out-of-range id and an over-full cell
-    bad1 = lays[0].copy(); bad1[0] = R * w.n_dp
-    lays = np.concatenate([lays, bad1[None]])
+    # infeasible layouts: an out-of-range id, a cell over capacity, an empty cell
+    bad = _infeasible_layouts(lays[0], w.lengths, R * w.n_dp, w.capacity)
+    lays = np.concatenate([lays, np.stack(bad)])
     prob = rp.Problem.from_dict(pd)
     out = rp.eval_objective(prob, w.lengths, q, R, lays, rank_load=load, want_J=True, want_diag=True)
     sc, st, J, dg = (out[k].cpu().numpy() for k in ("scores", "status", "J", "diag"))
@@ -112,6 +112,39 @@ def test_eval_objective(name, G, S):
         assert J[m].tolist() == oJ.tolist()
         if ost == 0:
             np.testing.assert_allclose(dg[m], odg, rtol=DIAG_RTOL, atol=0)
+    nb = len(bad)
+    assert st[-nb] & 1 and st[-nb + 1] & 2 and st[-nb + 2] & 4 and (st[:-nb] == 0).all()
+
+
+def _infeasible_layouts(lay, t, B, C):
+    """Three broken copies of a feasible layout: (1) a cell id out of range;
+    (2) a sample moved into the fullest cell it overflows, taken from a cell
+    that keeps a member; (3) every member of the smallest cell moved, first
+    fit, to other cells with room (else to the next cell)."""
+    t = np.asarray(t, dtype=np.int64)
+    bad1 = lay.copy()
+    bad1[0] = B
+    T = np.bincount(lay, weights=t, minlength=B).astype(np.int64)
+    n = np.bincount(lay, minlength=B)
+    order = np.argsort(-t, kind="stable")
+    bad2 = None
+    for c in np.argsort(-T, kind="stable"):
+        for i in order:
+            if lay[i] != c and n[lay[i]] >= 2 and T[c] + t[i] > C:
+                bad2 = lay.copy()
+                bad2[i] = c
+                break
+        if bad2 is not None:
+            break
+    assert bad2 is not None
+    a = int(np.argmin(T))
+    bad3 = lay.copy()
+    T3 = T.copy()
+    for i in np.flatnonzero(lay == a):
+        dest = next((c for c in range(B) if c != a and T3[c] + t[i] <= C), (a + 1) % B)
+        bad3[i] = dest
+        T3[dest] += t[i]
+    return [bad1, bad2, bad3]
 
 
 def _compare_anneal(g, o, steps=False):
@@ -456,6 +489,62 @@ def test_anneal_error_paths():
         rp.anneal(prob, w.lengths, q, pr["r_star"], pr["population"], [1e-3], 8, 1,
                   best_layout=pr["population"][0], best_score=np.array([1, 2, 3]))
     assert ei.value.code == -4
+
+
+@gpu
+@pytest.mark.parametrize("R", [512, 513])
+def test_anneal_row_shard_limit(R):
+    """R*G = 512 row-shards is the largest annealing shape (one sample per
+    cell, D = 1): it runs and equals the oracle; 513 is refused with
+    E_UNSUPPORTED before any device work."""
+    import oracle as O
+    rp = _rp()
+    rng = np.random.default_rng([5, R])
+    N, L, P = R, 1, 2
+    t = rng.integers(1, 100, size=N).astype(np.int32)
+    q = rng.integers(0, 50, size=(N, L, P)).astype(np.int32)
+    pd = dict(n_samples=N, n_layers=L, n_experts=P, top_k=1, n_ranks=P, n_dp=1, n_edp=1,
+              dp_to_edp=[0], capacity=128, alpha_fp=[4096], beta_fp=[1])
+    pop = np.tile(rng.permutation(N).astype(np.int32), (4, 1))
+    temps = [1e-3, 5e-4]
+    _log(f"anneal with R*G = {R}")
+    if R > 512:
+        with pytest.raises(rp.RoutepackError) as ei:
+            rp.anneal(rp.Problem.from_dict(pd), t, q, R, pop, temps, 32, 3)
+        assert ei.value.code == -8
+        return
+    g = rp.anneal(rp.Problem.from_dict(pd), t, q, R, pop, temps, 32, 3)
+    o = O.anneal(O.Problem.from_dict(pd), t, q, R, pop, temps, 32, 3)
+    assert o["rc"] == 0
+    _compare_anneal(g, o)
+
+
+@gpu
+def test_anneal_wait_gives_up_under_a_host_bound(monkeypatch):
+    """The whole-schedule kernel's barrier and hand-over waits poll a shared
+    error flag and give up after ROUTEPACK_WAIT_SPINS polls.  At the smallest
+    bound (32 polls, microseconds) the waits of a small-window level (tens of
+    microseconds of uneven member work) give up: every wave leaves the kernel
+    and the call returns E_DEVICE.  The next call, at the default bound, runs
+    normally and equals the oracle."""
+    import oracle as O
+    rp = _rp()
+    w, pd, pb, agg, slot, load, q = _window("small")
+    pr = _packed("small")
+    prob = rp.Problem.from_dict(pd)
+    temps = synth.anneal_temperatures(w.levels)[:6]
+    monkeypatch.setenv("ROUTEPACK_ANNEAL_KERNEL", "chain_run")
+    monkeypatch.setenv("ROUTEPACK_WAIT_SPINS", "32")
+    _log("anneal with 32-poll waits (expects E_DEVICE)")
+    with pytest.raises(rp.RoutepackError) as ei:
+        rp.anneal(prob, w.lengths, q, pr["r_star"], pr["population"], temps, 256, w.seed_anneal)
+    assert ei.value.code == -6
+    monkeypatch.delenv("ROUTEPACK_WAIT_SPINS")
+    _log("anneal again at the default bound")
+    g = rp.anneal(prob, w.lengths, q, pr["r_star"], pr["population"], temps, 256, w.seed_anneal)
+    assert g["level_kernel"] == "chain_run"
+    o = O.anneal(pb, w.lengths, q, pr["r_star"], pr["population"], temps, 256, w.seed_anneal)
+    _compare_anneal(g, o)
 
 
 @gpu
