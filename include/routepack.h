@@ -86,6 +86,21 @@ typedef struct routepack_problem {
 int routepack_aggregate_demand(const routepack_problem *prob, const int32_t *demand,
                                int64_t *agg, hipStream_t stream);
 
+/* routepack_aggregate_demand for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments and result; the band partials live in a fixed
+ * device array of 2^20 int64 (8 MiB) that the library holds on each device
+ * it runs on until the process ends, so the call allocates nothing (the
+ * first call on a device looks the array up with hipGetSymbolAddress).
+ * Every call on a device shares that array: calls that overlap on one device
+ * (on different streams, or from different threads) race and must be
+ * serialized by the caller.  Fewer, taller bands are used when the default
+ * band grid would not fit the array.  Asynchronous.  E_UNSUPPORTED when
+ * L * E > 2^20 (one band of partials would not fit); E_INVALID as
+ * routepack_aggregate_demand; E_DEVICE on a HIP error. */
+int routepack_aggregate_demand_noalloc(const routepack_problem *prob, const int32_t *demand,
+                                       int64_t *agg, hipStream_t stream);
+
 /* Layer-local LPT placement (Alg. 1), every layer independently: experts by
  * (-agg, e), each to the rank with fewer than H experts minimising
  * (G_p, p), taking slot p*H + n_p.  owner(v) = v / H.

@@ -153,6 +153,20 @@ def aggregate_demand(prob: Problem, demand):
     return agg
 
 
+def aggregate_demand_noalloc(prob: Problem, demand, out=None):
+    """aggregate_demand through routepack_aggregate_demand_noalloc: the
+    library allocates nothing (its partials live in a fixed device array);
+    `out` (int64 [L][E] on the device) receives the result when given."""
+    torch = _torch()
+    lib = load_library()
+    d = _dev(demand, torch.int32)
+    agg = out if out is not None else torch.empty((prob.n_layers, prob.n_experts), dtype=torch.int64,
+                                                  device="cuda")
+    _check("routepack_aggregate_demand_noalloc",
+           lib.routepack_aggregate_demand_noalloc(prob.ref, _ptr(d), _ptr(agg), _stream()))
+    return agg
+
+
 def place_experts(prob: Problem, agg, demand=None):
     """Layer-local LPT: returns (slot_of [L][E], rank_load [L][P], q [N][L][P] or None)."""
     torch = _torch()

@@ -9,12 +9,40 @@
 // one int64 partial per column and band.  A second kernel sums the bands of
 // each column (the partials are at most 2/64 of the bytes read).  Integer
 // sums are exact, so the result does not depend on the order.
+#include <mutex>
 #include <type_traits>
 
 #include "rp_device.h"
 #include "rp_internal.h"
 
 namespace rp {
+
+// Band partials of routepack_aggregate_demand_noalloc: a fixed device array
+// (each device the library runs on holds its own copy until the process
+// ends).  In host code `scratch` is only a stand-in for the symbol: its
+// device address comes from hipGetSymbolAddress, once per device.
+constexpr int64_t kAggScratchElems = (int64_t)1 << 20;  // 8 MiB of int64 partials
+static __device__ __align__(256) int64_t scratch[kAggScratchElems];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+int64_t *g_scratch_ptr[kMaxDevices];
+
+// The current device's address of `scratch` (looked up on the first call on
+// that device, with it current); nullptr on a HIP error.
+int64_t *agg_scratch_on_current_device() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+        g_scratch_ptr[dev] = static_cast<int64_t *>(ptr);
+    }
+    return g_scratch_ptr[dev];
+}
+}  // namespace
 
 __global__ void k_fill_i64(int64_t *p, int64_t n, int64_t v) {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
@@ -341,11 +369,15 @@ int launch_project(const int32_t *demand, const int32_t *eas, int32_t *q, int32_
 
 }  // namespace
 
-extern "C" int routepack_aggregate_demand(const routepack_problem *prob, const int32_t *demand,
-                                          int64_t *agg, hipStream_t stream) {
+// Both aggregation entry points: the band grid, then the two passes.  With
+// max_part > 0 the partials go to `fixed` (at most max_part int64 entries,
+// fewer bands when needed) instead of stream-ordered scratch.
+static int aggregate_demand(const routepack_problem *prob, const int32_t *demand, int64_t *agg,
+                            int64_t *fixed, int64_t max_part, hipStream_t stream) {
     if (!prob || !agg || (!demand && prob->n_samples > 0)) return ROUTEPACK_E_INVALID;
     if (prob->n_samples < 0 || prob->n_layers < 0 || prob->n_experts < 1) return ROUTEPACK_E_INVALID;
     const int64_t N = prob->n_samples, M = (int64_t)prob->n_layers * prob->n_experts;
+    if (max_part > 0 && M > max_part) return ROUTEPACK_E_UNSUPPORTED;  // not even one band fits
     if (M == 0) return ROUTEPACK_OK;
     if (N == 0) {
         hipLaunchKernelGGL(k_fill_i64, dim3((unsigned)((M + 255) / 256 < 1024 ? (M + 255) / 256 : 1024)),
@@ -358,12 +390,16 @@ extern "C" int routepack_aggregate_demand(const routepack_problem *prob, const i
     int64_t gy = (4096 + gx - 1) / gx, cap = N / 64 > 1 ? N / 64 : 1;
     if (gy > cap) gy = cap;
     if (gy > 65535) gy = 65535;
+    if (max_part > 0 && gy * M > max_part) gy = max_part / M;  // >= 1 (checked above)
     const int32_t band = (int32_t)((N + gy - 1) / gy);
     gy = (N + band - 1) / band;
     if (gx > 2147483647LL) return ROUTEPACK_E_UNSUPPORTED;
     Scratch scr(stream);
-    int64_t *part = scr.get<int64_t>((size_t)gy * M);
-    if (scr.failed()) return ROUTEPACK_E_DEVICE;
+    int64_t *part = fixed;
+    if (!part) {
+        part = scr.get<int64_t>((size_t)gy * M);
+        if (scr.failed()) return ROUTEPACK_E_DEVICE;
+    }
     if (vec)
         hipLaunchKernelGGL(k_aggregate_bands<4>, dim3((unsigned)gx, (unsigned)gy), dim3(256), 0, stream, demand,
                            part, (int32_t)N, M, band);
@@ -373,6 +409,21 @@ extern "C" int routepack_aggregate_demand(const routepack_problem *prob, const i
     hipLaunchKernelGGL(k_aggregate_cols, dim3((unsigned)((M + 63) / 64)), dim3(256), 0, stream,
                        (const int64_t *)part, (int32_t)gy, M, agg);
     return hipGetLastError() == hipSuccess ? ROUTEPACK_OK : ROUTEPACK_E_DEVICE;
+}
+
+extern "C" int routepack_aggregate_demand(const routepack_problem *prob, const int32_t *demand,
+                                          int64_t *agg, hipStream_t stream) {
+    return aggregate_demand(prob, demand, agg, nullptr, 0, stream);
+}
+
+extern "C" int routepack_aggregate_demand_noalloc(const routepack_problem *prob, const int32_t *demand,
+                                                  int64_t *agg, hipStream_t stream) {
+    if (!prob || !agg || (!demand && prob->n_samples > 0)) return ROUTEPACK_E_INVALID;
+    if (prob->n_layers < 0 || prob->n_experts < 1) return ROUTEPACK_E_INVALID;
+    if ((int64_t)prob->n_layers * prob->n_experts > kAggScratchElems) return ROUTEPACK_E_UNSUPPORTED;
+    int64_t *part = agg_scratch_on_current_device();
+    if (!part) return ROUTEPACK_E_DEVICE;
+    return aggregate_demand(prob, demand, agg, part, kAggScratchElems, stream);
 }
 
 extern "C" int routepack_place_experts(const routepack_problem *prob, const int64_t *agg,

@@ -17,7 +17,8 @@ def _declared(header="routepack.h"):
 
 
 def test_header_declares_the_boundary():
-    assert _declared() == sorted(["routepack_aggregate_demand", "routepack_place_experts",
+    assert _declared() == sorted(["routepack_aggregate_demand", "routepack_aggregate_demand_noalloc",
+                                  "routepack_place_experts",
                                   "routepack_pack_rows", "routepack_anneal",
                                   "routepack_eval_objective", "routepack_select_population",
                                   "routepack_row_lower_bound", "routepack_fixed_bin_search", "routepack_project_demand",
@@ -58,3 +59,13 @@ def test_invalid_problems_rejected_without_device_work():
                                 None, None) == -1
     assert lib.routepack_place_experts(bad.ref, None, None, None, None, None, None) == -1
     assert lib.routepack_aggregate_demand(None, None, None, None) == -1
+
+
+def test_noalloc_aggregation_rejects_oversized_shapes_without_device_work():
+    """routepack_aggregate_demand_noalloc refuses L E > 2^20 (one band of
+    partials would not fit its fixed array) before any HIP call."""
+    import paper_2608_12146_amd as rp
+    lib = rp.load_library()
+    big = rp.Problem(1, 1, (1 << 20) + 1, 1, 1, 1, 1, [0], 64, [4096], [1])
+    assert lib.routepack_aggregate_demand_noalloc(big.ref, C.c_void_p(16), C.c_void_p(16), None) == -8
+    assert lib.routepack_aggregate_demand_noalloc(None, None, None, None) == -1
