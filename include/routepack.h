@@ -185,7 +185,8 @@ typedef struct routepack_anneal_params {
  *              run in the same kernel): CHAIN shapes whose workgroups can
  *              all be resident at once
  *   CHAIN      one wave per member, lanes over (row-shard, layer) and cells:
- *              P in {4, 8, 16}, L <= 32, R G <= 64, <= 16 slots per shard
+ *              P in {4, 8, 16, 32}, L <= 32 (L <= 64 when P >= 16), R G <= 128
+ *              (<= 64 when P = 32), <= 16 slots per shard, N < 65536
  *   WAVE       one wave per member, lanes over flat 64-entry strides:
  *              R G <= 512, member state within LDS
  *   WORKGROUP  one workgroup per member, state in HBM: every problem within

@@ -3,10 +3,11 @@
 // 64-entry stride.
 //
 // Layout of a move's work over the 64 lanes:
-//  - W / q rows: lane (half, l) = (lane / 32, lane % 32) holds layer l of
-//    row-shard a (half 0) or b (half 1), all P ranks of that layer in
-//    registers, so the max over ranks is in-lane and only the sum over layers
-//    crosses lanes (one 16-lane DPP reduction per row-shard);
+//  - W / q rows: lane (half, l) = (lane / 32, lane % 32) holds layer l (and
+//    layer l + 32 when there are more than 32 layers) of row-shard a (half 0)
+//    or b (half 1), all P ranks of each layer in registers, so the max over
+//    ranks is in-lane and only the sum over layers crosses lanes (one 16-lane
+//    DPP reduction per row-shard);
 //  - cells: lane (half, x) with x < 16 holds the x-th cell of the row-shard,
 //    so both attention maxima and both cell-cost prefixes come from one
 //    16-lane DPP pass.
@@ -683,8 +684,9 @@ struct LevelOut {
 };
 
 // GV selects the variant: 1 the common shape (see screen), 0 the general
-// one, 2 the general one with two row-shards per lane (65 to 128).
-template <int PV, int DV, int GV>
+// one, 2 the general one with two row-shards per lane (65 to 128).  LV is
+// the number of layers per lane (2 for 33 to 64 layers).
+template <int PV, int DV, int GV, int LV>
 __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const Tables &tb, int32_t *W, int m,
                                         int32_t level, double temp, int64_t x0, int64_t x1, int64_t x2,
                                         uint8_t *log_arg, int64_t *res, int64_t *trace_row, Regs &R) {
@@ -709,24 +711,30 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
     int64_t n_acc = 0, n_eval = 0;
     double e_cur = GV == 1 ? energy_pow2(a, s0, s1, s2) : energy_k(a, s0, s1, s2);
     const int half = lane >> 5, hl = lane & 31, cx = lane & 15;
-    const bool lay_act = hl < L;  // lane holds layer hl of row-shard a / b
     const bool cell_lane = (lane & 16) == 0;
-    // Loads of one move: lane (half, hl) reads layer hl of row-shard ha
+    // layer v of the lane is hl + 32 v (v < LV), held when below L
+    auto lay_act = [&](int v) { return hl + 32 * v < L; };
+    // Loads of one move: lane (half, hl) reads its layers of row-shard ha
     // (half 0) or hb (half 1), the q row that leaves that row-shard (qx) and
     // the one that enters it (qy), so every lane's new row is wr - qx + qy.
     // A relocation moves no sample back: its missing row is the zero row.
     // Rows are chunk-major ([P/4][L][4]): chunk x of layer ll is int4 x * L + ll.
+    // Entry v * PV / 4 + x of wr, qx, qy is chunk x of the lane's layer v.
     auto load_rows = [&](int32_t i, int32_t j, int32_t ha, int32_t hb, int4 *wr, int4 *qx, int4 *qy) {
-        const int32_t row = half ? hb : ha, ll = lay_act ? hl : L - 1;
+        const int32_t row = half ? hb : ha;
         const int32_t *qi = a.qt + (int64_t)i * a.LP, *qj = j >= 0 ? a.qt + (int64_t)j * a.LP : a.qzero;
-        const int4 *wp = reinterpret_cast<const int4 *>(W + (int64_t)row * a.LP) + ll;
-        const int4 *xp = reinterpret_cast<const int4 *>(half ? qj : qi) + ll;
-        const int4 *yp = reinterpret_cast<const int4 *>(half ? qi : qj) + ll;
 #pragma unroll
-        for (int x = 0; x < PV / 4; ++x) {
-            wr[x] = wp[x * L];
-            qx[x] = xp[x * L];
-            qy[x] = yp[x * L];
+        for (int v = 0; v < LV; ++v) {
+            const int32_t ll = lay_act(v) ? hl + 32 * v : L - 1;
+            const int4 *wp = reinterpret_cast<const int4 *>(W + (int64_t)row * a.LP) + ll;
+            const int4 *xp = reinterpret_cast<const int4 *>(half ? qj : qi) + ll;
+            const int4 *yp = reinterpret_cast<const int4 *>(half ? qi : qj) + ll;
+#pragma unroll
+            for (int x = 0; x < PV / 4; ++x) {
+                wr[v * (PV / 4) + x] = wp[x * L];
+                qx[v * (PV / 4) + x] = xp[x * L];
+                qy[v * (PV / 4) + x] = yp[x * L];
+            }
         }
     };
 
@@ -780,7 +788,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
             const int32_t ha = ra * G + ga, hb = rb * G + gb;
             const bool two = ha != hb;
             // W rows of a and b, q rows of i and j: issue the loads first.
-            int4 wr[PV / 4], qx[PV / 4], qy[PV / 4];
+            int4 wr[LV * PV / 4], qx[LV * PV / 4], qy[LV * PV / 4];
             if (two) load_rows(i, j, ha, hb, wr, qx, qy);
             // Cell statistics of the two row-shards (lanes (half, cx)) and the
             // commit inputs, read in one stage while the row loads are in
@@ -839,25 +847,34 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
             const int64_t Jha = row_entry<RV>(Jr, Jr2, ha), Aha = row_entry<RV>(Ar, Ar2, ha);
             const int64_t Jhb = row_entry<RV>(Jr, Jr2, hb);
             int64_t Ja, Jb;
-            int32_t nw[PV];
+            int32_t nw[LV * PV];
             if (two) {
-                int32_t mx = INT32_MIN;
 #pragma unroll
-                for (int x = 0; x < PV / 4; ++x) {
+                for (int x = 0; x < LV * PV / 4; ++x) {
                     nw[4 * x + 0] = wr[x].x - qx[x].x + qy[x].x;
                     nw[4 * x + 1] = wr[x].y - qx[x].y + qy[x].y;
                     nw[4 * x + 2] = wr[x].z - qx[x].z + qy[x].z;
                     nw[4 * x + 3] = wr[x].w - qx[x].w + qy[x].w;
                 }
+                // the lane's share of the layer sum: the rank maximum of each
+                // of its layers (at most L W_b < 2^31 in the 32-bit case)
+                int32_t mx32 = 0;
+                int64_t mx64 = 0;
 #pragma unroll
-                for (int p = 0; p < PV; ++p) mx = nw[p] > mx ? nw[p] : mx;
+                for (int v = 0; v < LV; ++v) {
+                    int32_t mx = INT32_MIN;
+#pragma unroll
+                    for (int p = 0; p < PV; ++p) mx = nw[v * PV + p] > mx ? nw[v * PV + p] : mx;
+                    mx32 += lay_act(v) ? mx : 0;
+                    mx64 += lay_act(v) ? (int64_t)mx : 0;
+                }
                 int64_t suma, sumb;
                 if (GV == 1 || a.sum32) {  // L times the W bound fits 31 bits
-                    const int32_t sm = row_sum32(lay_act ? mx : 0);
+                    const int32_t sm = row_sum32(mx32);
                     suma = (int64_t)__builtin_amdgcn_readlane(sm, 0) + __builtin_amdgcn_readlane(sm, 16);
                     sumb = (int64_t)__builtin_amdgcn_readlane(sm, 32) + __builtin_amdgcn_readlane(sm, 48);
                 } else {
-                    const int64_t sm = row_sum64(lay_act ? (int64_t)mx : 0);
+                    const int64_t sm = row_sum64(mx64);
                     suma = (int64_t)(readlane64((uint64_t)sm, 0) + readlane64((uint64_t)sm, 16));
                     sumb = (int64_t)(readlane64((uint64_t)sm, 32) + readlane64((uint64_t)sm, 48));
                 }
@@ -935,11 +952,17 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
             n_acc += 1;
             // ---- commit
             wsync();
-            if (two && lay_act) {
-                int4 *wp = reinterpret_cast<int4 *>(W + (int64_t)(half ? hb : ha) * a.LP) + hl;
+            if (two) {
 #pragma unroll
-                for (int x = 0; x < PV / 4; ++x)
-                    wp[x * L] = make_int4(nw[4 * x], nw[4 * x + 1], nw[4 * x + 2], nw[4 * x + 3]);
+                for (int v = 0; v < LV; ++v) {
+                    if (!lay_act(v)) continue;
+                    int4 *wp = reinterpret_cast<int4 *>(W + (int64_t)(half ? hb : ha) * a.LP) + hl + 32 * v;
+#pragma unroll
+                    for (int x = 0; x < PV / 4; ++x) {
+                        const int y = v * PV + 4 * x;
+                        wp[x * L] = make_int4(nw[y], nw[y + 1], nw[y + 2], nw[y + 3]);
+                    }
+                }
             }
             if (!reloc) {
                 if (small) {
@@ -1084,10 +1107,14 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
 
 }  // namespace
 
+// Members per workgroup of the chain kernels (one wave each): four waves
+// leave every wave the whole register file of its SIMD.
+constexpr int kRunMaxWaves = 4;
+
 // One level of every member: state from the member's slab, K proposals,
 // state back to the slab.
-template <int PV, int DV, int GV>
-__global__ void __launch_bounds__(512) k_anneal_chain(AnnealArgs a) {
+template <int PV, int DV, int GV, int LV>
+__global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain(AnnealArgs a) {
     extern __shared__ __align__(16) char smem[];
     const Tables tb = load_tables(a, smem);
     const int wv = wave_id();
@@ -1097,7 +1124,7 @@ __global__ void __launch_bounds__(512) k_anneal_chain(AnnealArgs a) {
     const SlabPtrs g = slab_ptrs(a, a.slabs + (int64_t)a.slab_of[m] * a.off.bytes);
     Regs R;
     member_load<GV == 2 ? 2 : 1>(a, M, tb, g, R);
-    member_level<PV, DV, GV>(a, M, tb, g.W, m, a.level, a.temp, a.xscore[0], a.xscore[1], a.xscore[2],
+    member_level<PV, DV, GV, LV>(a, M, tb, g.W, m, a.level, a.temp, a.xscore[0], a.xscore[1], a.xscore[2],
                          a.step_log ? a.step_log + (int64_t)m * a.K : nullptr, a.results + (int64_t)m * kRes,
                          nullptr, R);
     member_store<GV == 2 ? 2 : 1>(a, M, g, R);
@@ -1317,7 +1344,6 @@ __device__ inline uint64_t block_excl_scan(uint64_t v, uint64_t *red, uint64_t *
 }  // namespace
 
 
-constexpr int kRunMaxWaves = 4;  // members per workgroup of the whole-schedule kernel
 
 namespace {
 
@@ -1344,7 +1370,7 @@ __device__ inline double wave_min_f64(double v) {
 
 }  // namespace
 
-template <int PV, int DV, int GV>
+template <int PV, int DV, int GV, int LV>
 __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(AnnealArgs a, RunArgs r) {
     extern __shared__ __align__(16) char smem[];
     __shared__ int64_t s_xs[3], s_k[kRunMaxWaves][4];
@@ -1388,7 +1414,7 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
         int64_t k0 = LLONG_MAX, k1 = LLONG_MAX, k2 = LLONG_MAX, kj = LLONG_MAX;
         double emin = __builtin_inf();
         if (active) {
-            const LevelOut lo = member_level<PV, DV, GV>(
+            const LevelOut lo = member_level<PV, DV, GV, LV>(
                 a, M, tb, g.W, m, level, temp, s_xs[0], s_xs[1], s_xs[2],
                 r.step_log ? r.step_log + ((int64_t)n * pop + m) * K : nullptr, a.results + (int64_t)m * kRes,
                 r.trace ? r.trace + ((int64_t)n * pop + m) * 8 : nullptr, R);
@@ -1638,7 +1664,7 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
 __global__ void __launch_bounds__(256) k_rows_to_chunks(const int32_t *src, int32_t *dst, int64_t n_rows,
                                                       int64_t row_stride, int64_t rows_per_group,
                                                       int64_t group_stride, int32_t L, int32_t P) {
-    __shared__ int32_t row[512];  // L * P <= 32 * 16
+    __shared__ int32_t row[2048];  // L * P <= 64 * 32
     const int64_t rr = blockIdx.x;
     if (rr >= n_rows) return;
     const int64_t off = (rr / rows_per_group) * group_stride + (rr % rows_per_group) * row_stride;
@@ -1652,7 +1678,7 @@ __global__ void __launch_bounds__(256) k_rows_to_chunks(const int32_t *src, int3
 }
 
 int chain_prepare(AnnealArgs &a, int32_t *qt, hipStream_t stream) {
-    if (a.L * a.P > 512 || (a.P & 3) != 0) return ROUTEPACK_E_UNSUPPORTED;
+    if (a.L * a.P > 2048 || (a.P & 3) != 0) return ROUTEPACK_E_UNSUPPORTED;
     if (a.LP > 0) {
         hipLaunchKernelGGL(k_rows_to_chunks, dim3((unsigned)a.N), dim3(256), 0, stream, a.q, qt, (int64_t)a.N,
                            (int64_t)a.LP, (int64_t)1, (int64_t)a.LP, a.L, a.P);
@@ -1670,11 +1696,15 @@ int chain_prepare(AnnealArgs &a, int32_t *qt, hipStream_t stream) {
 // shape (the caller then uses the flat wave kernel).
 bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out, int32_t *dv_out) {
     const int32_t P = a.P;
-    if (!(P == 4 || P == 8 || P == 16)) return false;
-    // (L >= 1: each move loads its rows with a layer on every lane of a half)
-    if (a.L < 1 || a.L > 32 || a.RG > 2 * kWave || max_count > 16 || a.N > 65535 || a.B + 1 > 65535 ||
-        a.C > 2147483647LL)
+    if (!(P == 4 || P == 8 || P == 16 || P == 32)) return false;
+    // (L >= 1: each move loads its rows with a layer on every lane of a half;
+    // 33 to 64 layers take two layers per lane, compiled for P >= 16)
+    if (a.L < 1 || a.L > 64 || (a.L > 32 && P < 16) || a.RG > 2 * kWave || max_count > 16 || a.N > 65535 ||
+        a.B + 1 > 65535 || a.C > 2147483647LL)
         return false;
+    // (32 ranks with two row-shards per lane are not compiled)
+    if (P == 32 && a.RG > kWave) return false;
+    a.lv = a.L > 32 ? 2 : 1;
     a.rv = a.RG > kWave ? 2 : 1;  // row-shards per lane
     const int32_t dv = max_count <= 8 ? 8 : 16;
     auto up16 = [](int64_t x) { return (x + 15) & ~(int64_t)15; };
@@ -1703,7 +1733,7 @@ bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out,
     const int64_t lim = 160 * 1024;
     if (shared + member > lim) return false;
     int64_t want = ((int64_t)a.pop + n_cu - 1) / n_cu;
-    want = want < 1 ? 1 : (want > 8 ? 8 : want);
+    want = want < 1 ? 1 : (want > kRunMaxWaves ? kRunMaxWaves : want);
     const int64_t cap = (lim - shared) / member;
     a.mpw = (int32_t)(want < cap ? want : cap);
     a.lds_shared = (int32_t)shared;
@@ -1713,14 +1743,14 @@ bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out,
     return true;
 }
 
-template <int PV, int DV, int GV>
+template <int PV, int DV, int GV, int LV>
 static int chain_launch_t(const AnnealArgs &a, hipStream_t stream) {
     const size_t lds = (size_t)a.lds_shared + (size_t)a.mpw * a.lds_member;
-    if (hipFuncSetAttribute((const void *)k_anneal_chain<PV, DV, GV>, hipFuncAttributeMaxDynamicSharedMemorySize,
+    if (hipFuncSetAttribute((const void *)k_anneal_chain<PV, DV, GV, LV>, hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)lds) != hipSuccess)
         return ROUTEPACK_E_DEVICE;
     const unsigned grid = (unsigned)((a.pop + a.mpw - 1) / a.mpw);
-    hipLaunchKernelGGL((k_anneal_chain<PV, DV, GV>), dim3(grid), dim3(kWave * a.mpw), lds, stream, a);
+    hipLaunchKernelGGL((k_anneal_chain<PV, DV, GV, LV>), dim3(grid), dim3(kWave * a.mpw), lds, stream, a);
     return hipGetLastError() == hipSuccess ? ROUTEPACK_OK : ROUTEPACK_E_DEVICE;
 }
 
@@ -1728,7 +1758,7 @@ static int chain_launch_t(const AnnealArgs &a, hipStream_t stream) {
 // or in HBM for the two-per-lane variant).
 int64_t run_lend_bytes(int32_t pop) { return (28 * (int64_t)pop + 255) & ~(int64_t)255; }
 
-template <int PV, int DV, int GV>
+template <int PV, int DV, int GV, int LV>
 static int chain_run_t(const AnnealArgs &a, const RunArgs &r0, int32_t n_cu, bool launch, hipStream_t stream) {
     RunArgs r = r0;
     if (a.mpw > kRunMaxWaves) return ROUTEPACK_E_UNSUPPORTED;
@@ -1738,7 +1768,7 @@ static int chain_run_t(const AnnealArgs &a, const RunArgs &r0, int32_t n_cu, boo
     // static LDS of the kernel is below 1 KiB
     if (lds + 1024 > 160 * 1024) return ROUTEPACK_E_UNSUPPORTED;
     r.o_lend = (int32_t)o_lend;
-    const void *fn = (const void *)k_anneal_chain_run<PV, DV, GV>;
+    const void *fn = (const void *)k_anneal_chain_run<PV, DV, GV, LV>;
     if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
         return ROUTEPACK_E_DEVICE;
     const int grid = (a.pop + a.mpw - 1) / a.mpw, block = kWave * a.mpw;
@@ -1761,11 +1791,33 @@ static int chain_variant(const AnnealArgs &a, bool step_log) {
     return a.G == 1 && a.dshift >= 0 && a.S == 1 && a.sum32 && a.scale_pow2 && !step_log ? 1 : 0;
 }
 
-template <int PV, int DV>
+template <int PV, int DV, int LV>
 static int chain_run_v(int v, const AnnealArgs &a, const RunArgs &r, int32_t n_cu, bool launch, hipStream_t stream) {
-    if (v == 2) return chain_run_t<PV, DV, 2>(a, r, n_cu, launch, stream);
-    if (v == 1) return chain_run_t<PV, DV, 1>(a, r, n_cu, launch, stream);
-    return chain_run_t<PV, DV, 0>(a, r, n_cu, launch, stream);
+    if (v == 2) {
+        if constexpr (PV == 32) return ROUTEPACK_E_UNSUPPORTED;  // (excluded by chain_plan)
+        else return chain_run_t<PV, DV, 2, LV>(a, r, n_cu, launch, stream);
+    }
+    if (v == 1) return chain_run_t<PV, DV, 1, LV>(a, r, n_cu, launch, stream);
+    return chain_run_t<PV, DV, 0, LV>(a, r, n_cu, launch, stream);
+}
+
+template <int DV>
+static int chain_run_d(int v, const AnnealArgs &a, const RunArgs &r, int32_t pv, int32_t n_cu, bool launch,
+                       hipStream_t stream) {
+    if (a.lv == 2) {
+        switch (pv) {
+            case 16: return chain_run_v<16, DV, 2>(v, a, r, n_cu, launch, stream);
+            case 32: return chain_run_v<32, DV, 2>(v, a, r, n_cu, launch, stream);
+        }
+        return ROUTEPACK_E_UNSUPPORTED;
+    }
+    switch (pv) {
+        case 4: return chain_run_v<4, DV, 1>(v, a, r, n_cu, launch, stream);
+        case 8: return chain_run_v<8, DV, 1>(v, a, r, n_cu, launch, stream);
+        case 16: return chain_run_v<16, DV, 1>(v, a, r, n_cu, launch, stream);
+        case 32: return chain_run_v<32, DV, 1>(v, a, r, n_cu, launch, stream);
+    }
+    return ROUTEPACK_E_UNSUPPORTED;
 }
 
 // Checks (launch = false) or launches (launch = true) the whole-schedule
@@ -1773,45 +1825,41 @@ static int chain_run_v(int v, const AnnealArgs &a, const RunArgs &r, int32_t n_c
 int chain_run(const AnnealArgs &a, const RunArgs &r, int32_t pv, int32_t dv, int32_t n_cu, bool launch,
               hipStream_t stream) {
     const int v = chain_variant(a, r.step_log != nullptr);
-    if (dv == 8) {
-        switch (pv) {
-            case 4: return chain_run_v<4, 8>(v, a, r, n_cu, launch, stream);
-            case 8: return chain_run_v<8, 8>(v, a, r, n_cu, launch, stream);
-            case 16: return chain_run_v<16, 8>(v, a, r, n_cu, launch, stream);
-        }
-    } else {
-        switch (pv) {
-            case 4: return chain_run_v<4, 16>(v, a, r, n_cu, launch, stream);
-            case 8: return chain_run_v<8, 16>(v, a, r, n_cu, launch, stream);
-            case 16: return chain_run_v<16, 16>(v, a, r, n_cu, launch, stream);
-        }
-    }
-    return ROUTEPACK_E_UNSUPPORTED;
+    return dv == 8 ? chain_run_d<8>(v, a, r, pv, n_cu, launch, stream)
+                   : chain_run_d<16>(v, a, r, pv, n_cu, launch, stream);
 }
 
-template <int PV, int DV>
+template <int PV, int DV, int LV>
 static int chain_launch_v(int v, const AnnealArgs &a, hipStream_t stream) {
-    if (v == 2) return chain_launch_t<PV, DV, 2>(a, stream);
-    if (v == 1) return chain_launch_t<PV, DV, 1>(a, stream);
-    return chain_launch_t<PV, DV, 0>(a, stream);
+    if (v == 2) {
+        if constexpr (PV == 32) return ROUTEPACK_E_UNSUPPORTED;  // (excluded by chain_plan)
+        else return chain_launch_t<PV, DV, 2, LV>(a, stream);
+    }
+    if (v == 1) return chain_launch_t<PV, DV, 1, LV>(a, stream);
+    return chain_launch_t<PV, DV, 0, LV>(a, stream);
+}
+
+template <int DV>
+static int chain_launch_d(int v, const AnnealArgs &a, int32_t pv, hipStream_t stream) {
+    if (a.lv == 2) {
+        switch (pv) {
+            case 16: return chain_launch_v<16, DV, 2>(v, a, stream);
+            case 32: return chain_launch_v<32, DV, 2>(v, a, stream);
+        }
+        return ROUTEPACK_E_UNSUPPORTED;
+    }
+    switch (pv) {
+        case 4: return chain_launch_v<4, DV, 1>(v, a, stream);
+        case 8: return chain_launch_v<8, DV, 1>(v, a, stream);
+        case 16: return chain_launch_v<16, DV, 1>(v, a, stream);
+        case 32: return chain_launch_v<32, DV, 1>(v, a, stream);
+    }
+    return ROUTEPACK_E_UNSUPPORTED;
 }
 
 int launch_anneal_chain(const AnnealArgs &a, int32_t pv, int32_t dv, hipStream_t stream) {
     const int v = chain_variant(a, a.step_log != nullptr);
-    if (dv == 8) {
-        switch (pv) {
-            case 4: return chain_launch_v<4, 8>(v, a, stream);
-            case 8: return chain_launch_v<8, 8>(v, a, stream);
-            case 16: return chain_launch_v<16, 8>(v, a, stream);
-        }
-    } else {
-        switch (pv) {
-            case 4: return chain_launch_v<4, 16>(v, a, stream);
-            case 8: return chain_launch_v<8, 16>(v, a, stream);
-            case 16: return chain_launch_v<16, 16>(v, a, stream);
-        }
-    }
-    return ROUTEPACK_E_UNSUPPORTED;
+    return dv == 8 ? chain_launch_d<8>(v, a, pv, stream) : chain_launch_d<16>(v, a, pv, stream);
 }
 
 }  // namespace rp

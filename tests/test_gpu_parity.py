@@ -242,6 +242,43 @@ def test_anneal_two_stages(kernel, monkeypatch):
         _compare_anneal(g, o)
 
 
+# Shapes with more than 32 layers (two layers per lane in the chain kernels)
+# and 32 ranks (the heavy-tail window's rank count), one and two EDP shards.
+MANY_LAYERS = {
+    "l40_p32": dict(n=160, layers=40, experts=64, top_k=8, ranks=32, dp=4, edp=1),
+    "l40_p16_g2": dict(n=160, layers=40, experts=64, top_k=8, ranks=16, dp=4, edp=2),
+    "l64_p32": dict(n=96, layers=64, experts=64, top_k=8, ranks=32, dp=8, edp=1),
+    "l24_p32": dict(n=120, layers=24, experts=64, top_k=8, ranks=32, dp=4, edp=1),
+}
+
+
+@gpu
+@pytest.mark.parametrize("kernel", KERNELS)
+@pytest.mark.parametrize("case", sorted(MANY_LAYERS))
+def test_anneal_many_layers(case, kernel, monkeypatch):
+    """Full trajectories (12 levels of 256 proposals, population 32) on shapes
+    beyond 32 layers or 16 ranks, on every annealing kernel."""
+    import oracle as O
+    rp = _rp()
+    _use_kernel(monkeypatch, kernel)
+    w = synth.make_tiny_random(60 + sorted(MANY_LAYERS).index(case), cap=4096, tmin=64, tmax=1500, pop=32,
+                               levels=12, **MANY_LAYERS[case])
+    pd = synth.window_problem(w)
+    pb = O.Problem.from_dict(pd)
+    slot, _ = O.place(O.aggregate(w.demand), w.n_ranks)
+    q = O.project(w.demand, slot, w.n_ranks)
+    pr = O.pack_rows(pb, w.lengths, q, w.seed_pack, 8, 3, w.pop)
+    assert pr["rc"] == 0
+    temps = synth.anneal_temperatures(w.levels)
+    _log(f"anneal {case}: R={pr['r_star']}, {w.levels} levels, {kernel} kernel")
+    o = O.anneal(pb, w.lengths, q, pr["r_star"], pr["population"], temps, 256, w.seed_anneal)
+    assert o["rc"] == 0
+    g = rp.anneal(rp.Problem.from_dict(pd), w.lengths, q, pr["r_star"], pr["population"], temps, 256,
+                  w.seed_anneal)
+    assert g["level_kernel"] == kernel
+    _compare_anneal(g, o)
+
+
 # Degenerate shapes: no MoE layer (the rows are empty), a population that
 # fills no workgroup, a level size that is not a multiple of the batch of 64,
 # one DP slot, one proposal per level, and one row of two one-sample cells
