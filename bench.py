@@ -303,6 +303,8 @@ def main():
     ap.add_argument("--cpu-levels", type=int, default=None,
                     help="levels the oracle runs after the timed region (default: the whole schedule, "
                          "whose trajectory is then compared with the last timed step's)")
+    ap.add_argument("--no-extra-windows", action="store_true",
+                    help="skip the short heavy-tail and stress runs reported under extra_windows")
     ap.add_argument("--print-maps", action="store_true",
                     help="print /proc/self/maps to stderr before exiting (to attribute exit-time faults)")
     ap.add_argument("--copy-probe", action="store_true")
@@ -487,6 +489,15 @@ def main():
             traj["best_score_eq_oracle"] = an["best_score"].cpu().tolist() == oc["best_score"].tolist()
         progress(f"oracle: {cev} evaluated moves in {tcpu:.1f} s; trajectory == GPU {traj}")
 
+    extra = None
+    if not args.no_extra_windows and args.window == "mid":
+        extra = {}
+        for name, nl in (("heavy", 20), ("stress", 3)):
+            progress(f"extra window {name}: {nl} levels")
+            extra[name] = window_short_run(name, nl)
+            progress(f"  {extra[name]['kernel']}: {extra[name]['move_evals_per_s_kernel']:.3e} move-evals/s "
+                     f"(kernel), roofline {extra[name]['roofline']['frac']:.4f}, parity {extra[name]['parity']}")
+
     out = {
         "metric": "anneal move-evals/sec; objective==oracle; % HBM/LDS roofline",
         "value": evals / dt,
@@ -517,10 +528,63 @@ def main():
         "row_lower_bound": row_bound,
         "fixed_bin_search": search,
         "demand_stream": dstream,
+        "extra_windows": extra,
         "r_star": pk["r_star"],
         "best_score": an["best_score"].cpu().tolist(),
     }
     print(json.dumps(out), flush=True)
+
+
+def window_short_run(name, levels):
+    """The annealing path on another benchmark window for its first `levels`
+    levels (full population, the window's own schedule): the level kernel the
+    library picks, its rate over the kernel time (HIP events around each
+    launch, second of two runs), the HBM roofline fraction by the same
+    algorithmic bytes as the main line, and the oracle's check of three
+    members' first level and of x*."""
+    import torch
+
+    import oracle as O
+    import paper_2608_12146_amd as rp
+    import synth
+    from synth import windows as W
+    w = synth.make_window(name)
+    pd = synth.window_problem(w)
+    prob = rp.Problem.from_dict(pd)
+    demand = torch.as_tensor(w.demand, device="cuda")
+    lengths = torch.as_tensor(w.lengths, device="cuda")
+    agg = rp.aggregate_demand(prob, demand)
+    slot, load, q = rp.place_experts(prob, agg, demand)
+    del demand
+    pk = rp.pack_rows(prob, lengths, q, w.seed_pack, W.N_TRIALS, W.CHOICE_WIDTH, w.pop)
+    temps = synth.anneal_temperatures(w.levels)
+    K = W.STEPS_PER_LEVEL
+    for _ in range(2):
+        an = rp.anneal(prob, lengths, q, pk["r_star"], pk["population"], temps[:levels], K, w.seed_anneal,
+                       t_next=temps[levels], want_parents=False, kernel_times=True)
+        torch.cuda.synchronize()
+    tr = an["trace"].cpu().numpy()
+    evals = int(tr[:, :, 7].sum())
+    k_ms = float(an["level_kernel_ms"].sum())
+    bytes_per_eval = (2.0 - W.RHO_U32 / 2.0**32) * w.n_layers * w.n_ranks * 4
+    rate = evals / (k_ms / 1e3)
+    pb = O.Problem.from_dict(pd)
+    qn = q.cpu().numpy()
+    ids = np.array([0, w.pop // 2, w.pop - 1], dtype=np.int32)
+    oa = O.anneal(pb, w.lengths, qn, pk["r_star"], pk["population"].cpu().numpy()[ids], temps[:1], K,
+                  w.seed_anneal, replica_ids=ids)
+    st, s_or, _, _ = O.score(pb, w.lengths, qn, pk["r_star"], an["best_layout"].cpu().numpy())
+    out = {"workload": workload_text(w, 1), "levels": levels, "kernel": "k_anneal_" + an["level_kernel"],
+           "evals": evals, "kernel_ms": k_ms, "move_evals_per_s_kernel": rate,
+           "roofline": {"bound": "hbm", "achieved": rate * bytes_per_eval / 1e9, "peak": HBM_PEAK_GBS,
+                        "unit": "GB/s", "frac": rate * bytes_per_eval / 1e9 / HBM_PEAK_GBS,
+                        "bytes_per_eval": bytes_per_eval},
+           "parity": {"level0_sampled_members_eq_oracle": bool(oa["rc"] == 0 and
+                                                               np.array_equal(tr[0][ids], oa["trace"][0])),
+                      "x_star_rescored_eq_oracle": bool(st == 0 and
+                                                        s_or.tolist() == an["best_score"].cpu().tolist())}}
+    del q, an, pk
+    return out
 
 
 def release_device_state():
