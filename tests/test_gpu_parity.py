@@ -249,6 +249,8 @@ MANY_LAYERS = {
     "l40_p16_g2": dict(n=160, layers=40, experts=64, top_k=8, ranks=16, dp=4, edp=2),
     "l64_p32": dict(n=96, layers=64, experts=64, top_k=8, ranks=32, dp=8, edp=1),
     "l24_p32": dict(n=120, layers=24, experts=64, top_k=8, ranks=32, dp=4, edp=1),
+    # more than 64 row-shards: two row-shards and two layers per lane
+    "l40_p16_rg68": dict(n=250, layers=40, experts=64, top_k=8, ranks=16, dp=2, edp=2, cap=1600, tmax=800),
 }
 
 
@@ -261,8 +263,9 @@ def test_anneal_many_layers(case, kernel, monkeypatch):
     import oracle as O
     rp = _rp()
     _use_kernel(monkeypatch, kernel)
-    w = synth.make_tiny_random(60 + sorted(MANY_LAYERS).index(case), cap=4096, tmin=64, tmax=1500, pop=32,
-                               levels=12, **MANY_LAYERS[case])
+    shape = dict(cap=4096, tmin=64, tmax=1500, pop=32, levels=12)
+    shape.update(MANY_LAYERS[case])
+    w = synth.make_tiny_random(60 + sorted(MANY_LAYERS).index(case), **shape)
     pd = synth.window_problem(w)
     pb = O.Problem.from_dict(pd)
     slot, _ = O.place(O.aggregate(w.demand), w.n_ranks)
