@@ -186,7 +186,12 @@ typedef struct routepack_anneal_params {
  *              all be resident at once
  *   CHAIN      one wave per member, lanes over (row-shard, layer) and cells:
  *              P in {4, 8, 16, 32}, L <= 32 (L <= 64 when P >= 16), R G <= 128
- *              (<= 64 when P = 32), <= 16 slots per shard, N < 65536
+ *              (<= 64 when P = 32), <= 16 slots per shard, N < 65536.  When
+ *              the population cannot be resident at once and P = 32, the
+ *              per-level launch may keep each member's cell array and the
+ *              lengths in HBM to fit more members per CU
+ *              (ROUTEPACK_CHAIN_LAYOUT=hbm asks for that layout, =lds
+ *              forbids it)
  *   WAVE       one wave per member, lanes over flat 64-entry strides:
  *              R G <= 512, member state within LDS
  *   WORKGROUP  one workgroup per member, state in HBM: every problem within

@@ -51,6 +51,7 @@ struct AnnealArgs {
     int32_t dshift;             // chain kernel: log2 D when D is a power of two, else -1
     int32_t rv;                 // chain kernel: row-shards per lane (1 up to 64 row-shards, 2 up to 128)
     int32_t lv;                 // chain kernel: layers per lane (1 up to 32 layers, 2 up to 64)
+    int32_t cg;                 // chain kernel: the cell array and the lengths stay in HBM, not LDS
     int32_t dv, o_hcnt, o_hcell;  // chain kernel: cost-prefix stride; row-shard slot tables (shared)
     int32_t scale_pow2;         // 2^F C is a power of two
     double inv_scale;           // 1 / (2^F C) when it is

@@ -22,6 +22,9 @@
 // The sequence of evaluated proposals, accept decisions and states is the
 // sequential one (a rejected proposal leaves every screen valid, an accepted
 // one triggers a re-screen of the rest of the batch).
+#include <cstdlib>
+#include <cstring>
+
 #include "rp_anneal.h"
 
 namespace rp {
@@ -61,6 +64,7 @@ __device__ inline int64_t row_head_max64(int64_t v) {
 
 struct Lds {
     uint16_t *cell, *pool, *start;
+    int32_t *gcell;  // the cell array in the member's slab instead (CG layout)
     int32_t *T;
     int64_t *Q;
     // [RG][DV + 1] prefix of the cell costs of each row-shard, slot order;
@@ -149,6 +153,13 @@ __device__ inline void stage_end(T &...v) {
     (stage_one(v), ...);
 }
 
+// Cell of sample i: in LDS, or (CG layout) in the member's slab.
+template <bool CG>
+__device__ inline int32_t cell_of(const Lds &M, int32_t i) {
+    if constexpr (CG) return M.gcell[i];
+    else return M.cell[i];
+}
+
 // Resolves the proposal of this lane against the member's current state.
 // The reads go out in dependent stages; the uniform-mode proposal's reads
 // ride along with the first two stages of the guided chain.  GV == 1 is the
@@ -156,7 +167,7 @@ __device__ inline void stage_end(T &...v) {
 // count D, one attention stage (S == 1), 32-bit layer sums, a power-of-two
 // score scale and no step log; GV == 0 takes all of these from the arguments.
 // RV is the number of row-shards per lane (2 for 65 to 128 row-shards).
-template <int DV, int GV, int RV>
+template <int DV, int GV, int RV, bool CG>
 __device__ inline Screen screen(const AnnealArgs &a, const Lds &M, const Tables &tb, uint64_t w0, uint64_t w1,
                                 uint64_t w2, uint64_t w3, uint64_t w4, uint64_t w5, uint64_t w6, int64_t s1,
                                 int64_t s2) {
@@ -183,7 +194,7 @@ __device__ inline Screen screen(const AnnealArgs &a, const Lds &M, const Tables 
         jp[k] = M.Jpiv[k];
         vp[k] = M.Vpiv[k];
     }
-    int32_t cir = M.cell[ir], cjr = M.cell[jr];
+    int32_t cir = cell_of<CG>(M, ir), cjr = cell_of<CG>(M, jr);
     int32_t tir = tb.t[ir], tjr = tb.t[jr];
 #pragma unroll
     for (int k = 0; k < NP; ++k) stage_end(jp[k], vp[k]);
@@ -518,6 +529,10 @@ __device__ inline Tables load_tables(const AnnealArgs &a, char *smem) {
         if (k == 0) s_hcnt[h] = cnt;
         s_hcell[x] = r * D + a.slots[g * D + (k < cnt ? k : cnt - 1)];
     }
+    if (a.cg) {  // the lengths are read from HBM (L2)
+        __syncthreads();
+        return Tables{s_slots, s_count, s_shard, s_soff, a.t, s_hcnt, s_hcell};
+    }
     const int32_t n4 = N >> 2;
     const int4 *t4 = reinterpret_cast<const int4 *>(a.t);
     for (int32_t x = threadIdx.x; x < n4; x += blockDim.x) reinterpret_cast<int4 *>(s_t)[x] = t4[x];
@@ -562,7 +577,7 @@ __device__ inline void member_load(const AnnealArgs &a, const Lds &M, const Tabl
             for (int u = 0; u < U; ++u) {
                 const int32_t x = base + u * kWave + lane;
                 if (x < n4) {
-                    cu[u] = c4[x];
+                    if (!a.cg) cu[u] = c4[x];  // (CG layout: the cell array stays in the slab)
                     pu[u] = p4[x];
                 }
             }
@@ -570,13 +585,15 @@ __device__ inline void member_load(const AnnealArgs &a, const Lds &M, const Tabl
             for (int u = 0; u < U; ++u) {
                 const int32_t x = base + u * kWave + lane;
                 if (x < n4) {
-                    lc4[x] = make_ushort4((uint16_t)cu[u].x, (uint16_t)cu[u].y, (uint16_t)cu[u].z, (uint16_t)cu[u].w);
+                    if (!a.cg)
+                        lc4[x] = make_ushort4((uint16_t)cu[u].x, (uint16_t)cu[u].y, (uint16_t)cu[u].z,
+                                              (uint16_t)cu[u].w);
                     lp4[x] = make_ushort4((uint16_t)pu[u].x, (uint16_t)pu[u].y, (uint16_t)pu[u].z, (uint16_t)pu[u].w);
                 }
             }
         }
         for (int32_t x = (n4 << 2) + lane; x < N; x += kWave) {
-            M.cell[x] = (uint16_t)g.cell[x];
+            if (!a.cg) M.cell[x] = (uint16_t)g.cell[x];
             M.pool[x] = (uint16_t)g.pool[x];
         }
     }
@@ -651,12 +668,15 @@ __device__ inline void member_store(const AnnealArgs &a, const Lds &M, const Sla
     int4 *c4 = reinterpret_cast<int4 *>(g.cell), *p4 = reinterpret_cast<int4 *>(g.pool);
     const ushort4 *lc4 = reinterpret_cast<const ushort4 *>(M.cell), *lp4 = reinterpret_cast<const ushort4 *>(M.pool);
     for (int32_t x = lane; x < n4; x += kWave) {
-        const ushort4 u = lc4[x], v = lp4[x];
-        c4[x] = make_int4(u.x, u.y, u.z, u.w);
+        const ushort4 v = lp4[x];
+        if (!a.cg) {  // (CG layout: the slab's cell array is already current)
+            const ushort4 u = lc4[x];
+            c4[x] = make_int4(u.x, u.y, u.z, u.w);
+        }
         p4[x] = make_int4(v.x, v.y, v.z, v.w);
     }
     for (int32_t x = (n4 << 2) + lane; x < N; x += kWave) {
-        g.cell[x] = M.cell[x];
+        if (!a.cg) g.cell[x] = M.cell[x];
         g.pool[x] = M.pool[x];
     }
     for (int32_t x = lane; x <= B; x += kWave) g.start[x] = M.start[x];
@@ -686,7 +706,7 @@ struct LevelOut {
 // GV selects the variant: 1 the common shape (see screen), 0 the general
 // one, 2 the general one with two row-shards per lane (65 to 128).  LV is
 // the number of layers per lane (2 for 33 to 64 layers).
-template <int PV, int DV, int GV, int LV>
+template <int PV, int DV, int GV, int LV, bool CG>
 __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const Tables &tb, int32_t *W, int m,
                                         int32_t level, double temp, int64_t x0, int64_t x1, int64_t x2,
                                         uint8_t *log_arg, int64_t *res, int64_t *trace_row, Regs &R) {
@@ -705,7 +725,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
     if (lex_less(s0, s1, s2, x0, x1, x2)) {
         // A start state better than the incumbent is itself a trajectory
         // best; keep its layout, since the state is updated in place.
-        for (int32_t x = lane; x < N; x += kWave) bl[x] = M.cell[x];
+        for (int32_t x = lane; x < N; x += kWave) bl[x] = cell_of<CG>(M, x);
         best_is_start = 0;
     }
     int64_t n_acc = 0, n_eval = 0;
@@ -747,7 +767,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
         const uint64_t w0 = b0w.v[0], w1 = b0w.v[1], w2 = b0w.v[2], w3 = b0w.v[3];
         const uint64_t w4 = b1w.v[0], w5 = b1w.v[1], w6 = b1w.v[2], w7 = b1w.v[3];
         uint64_t pending = __ballot(k < a.K);
-        Screen sc = screen<DV, GV, RV>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
+        Screen sc = screen<DV, GV, RV, CG>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
         uint64_t feas = __ballot(sc.feas && k < a.K);
         uint64_t valid = ~0ull;  // lanes whose screen is current
         while (pending) {
@@ -757,7 +777,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                 // current; otherwise screen the batch again.
                 const uint64_t stale = pending & ~valid;
                 if (stale && (!cand || (stale & (~stale + 1)) <= (cand & (~cand + 1)))) {
-                    sc = screen<DV, GV, RV>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
+                    sc = screen<DV, GV, RV, CG>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
                     feas = __ballot(sc.feas && k < a.K);
                     valid = ~0ull;
                     cand = pending & feas;
@@ -1003,8 +1023,13 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                 else start_add(M.start, c2, c1, 1);
             }
             if (lane == 0) {
-                M.cell[i] = (uint16_t)c2;
-                if (j >= 0) M.cell[j] = (uint16_t)c1;
+                if constexpr (CG) {
+                    M.gcell[i] = c2;
+                    if (j >= 0) M.gcell[j] = c1;
+                } else {
+                    M.cell[i] = (uint16_t)c2;
+                    if (j >= 0) M.cell[j] = (uint16_t)c1;
+                }
                 M.T[c1] = (int32_t)nT1;
                 M.Q[c1] = nQ1;
                 M.T[c2] = (int32_t)nT2;
@@ -1076,7 +1101,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                 b2 = s2;
                 best_is_start = 0;
                 if (lex_less(s0, s1, s2, x0, x1, x2))
-                    for (int32_t x = lane; x < N; x += kWave) bl[x] = M.cell[x];
+                    for (int32_t x = lane; x < N; x += kWave) bl[x] = cell_of<CG>(M, x);
             }
         }
     }
@@ -1113,18 +1138,19 @@ constexpr int kRunMaxWaves = 4;
 
 // One level of every member: state from the member's slab, K proposals,
 // state back to the slab.
-template <int PV, int DV, int GV, int LV>
+template <int PV, int DV, int GV, int LV, bool CG>
 __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain(AnnealArgs a) {
     extern __shared__ __align__(16) char smem[];
     const Tables tb = load_tables(a, smem);
     const int wv = wave_id();
     const int m = blockIdx.x * a.mpw + wv;
     if (m >= a.pop) return;  // no block barrier follows
-    const Lds M = member_lds(a, smem, wv);
+    Lds M = member_lds(a, smem, wv);
     const SlabPtrs g = slab_ptrs(a, a.slabs + (int64_t)a.slab_of[m] * a.off.bytes);
+    M.gcell = g.cell;
     Regs R;
     member_load<GV == 2 ? 2 : 1>(a, M, tb, g, R);
-    member_level<PV, DV, GV, LV>(a, M, tb, g.W, m, a.level, a.temp, a.xscore[0], a.xscore[1], a.xscore[2],
+    member_level<PV, DV, GV, LV, CG>(a, M, tb, g.W, m, a.level, a.temp, a.xscore[0], a.xscore[1], a.xscore[2],
                          a.step_log ? a.step_log + (int64_t)m * a.K : nullptr, a.results + (int64_t)m * kRes,
                          nullptr, R);
     member_store<GV == 2 ? 2 : 1>(a, M, g, R);
@@ -1414,7 +1440,7 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
         int64_t k0 = LLONG_MAX, k1 = LLONG_MAX, k2 = LLONG_MAX, kj = LLONG_MAX;
         double emin = __builtin_inf();
         if (active) {
-            const LevelOut lo = member_level<PV, DV, GV, LV>(
+            const LevelOut lo = member_level<PV, DV, GV, LV, false>(
                 a, M, tb, g.W, m, level, temp, s_xs[0], s_xs[1], s_xs[2],
                 r.step_log ? r.step_log + ((int64_t)n * pop + m) * K : nullptr, a.results + (int64_t)m * kRes,
                 r.trace ? r.trace + ((int64_t)n * pop + m) * 8 : nullptr, R);
@@ -1707,34 +1733,59 @@ bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out,
     a.lv = a.L > 32 ? 2 : 1;
     a.rv = a.RG > kWave ? 2 : 1;  // row-shards per lane
     const int32_t dv = max_count <= 8 ? 8 : 16;
-    auto up16 = [](int64_t x) { return (x + 15) & ~(int64_t)15; };
-    auto up8e = [](int64_t n) { return ((n + 7) & ~(int64_t)7) + 16; };  // elements, padded for 16-byte steps
-    int64_t o = 0;
-    a.o_cell = (int32_t)o; o = up16(o + 2 * (int64_t)a.N);
-    a.o_pool = (int32_t)o; o = up16(o + 2 * up8e(a.N));
-    a.o_start = (int32_t)o; o = up16(o + 2 * up8e((int64_t)a.B + 1));
-    a.o_T = (int32_t)o; o = up16(o + 4 * (int64_t)a.B);
-    a.o_Q = (int32_t)o; o = up16(o + 8 * (int64_t)a.B);
     a.dv = dv;
-    a.o_acost = (int32_t)o; o = up16(o + 8 * ((int64_t)a.RG * (dv + 1) + a.RG));  // cost prefixes and totals
-    a.o_Jpre = (int32_t)o; o = up16(o + 8 * 144 * (int64_t)a.rv);  // J_pre, V_pre and their pivots
-    a.o_Jpiv = a.o_Jpre + 8 * 128 * a.rv;
     a.ginv = (uint32_t)((((uint64_t)1 << 32) + (uint64_t)a.G - 1) / (uint64_t)a.G);
     a.dinv = (uint32_t)((((uint64_t)1 << 32) + (uint64_t)a.D - 1) / (uint64_t)a.D);
     a.dshift = -1;
     for (int32_t sh = 0; sh < 16; ++sh)
         if ((1 << sh) == a.D) a.dshift = sh;
-    const int64_t member = o;
-    int64_t tab = up16(4 * ((int64_t)a.G * a.D + 2 * a.G + a.D));
-    a.o_hcnt = (int32_t)tab; tab = up16(tab + 4 * (int64_t)a.RG);
-    a.o_hcell = (int32_t)tab; tab = up16(tab + 4 * (int64_t)a.RG * dv);
-    a.o_tshared = (int32_t)tab;
-    const int64_t shared = up16(tab + 4 * (int64_t)a.N);
+    auto up16 = [](int64_t x) { return (x + 15) & ~(int64_t)15; };
+    auto up8e = [](int64_t n) { return ((n + 7) & ~(int64_t)7) + 16; };  // elements, padded for 16-byte steps
+    // LDS of one member and of the workgroup's shared tables; with cg the
+    // cell array stays in the slab and the lengths are read from HBM.
+    auto layout = [&](bool cg, int64_t *shared_out) -> int64_t {
+        int64_t o = 0;
+        a.o_cell = (int32_t)o; o = up16(o + (cg ? 0 : 2 * (int64_t)a.N));
+        a.o_pool = (int32_t)o; o = up16(o + 2 * up8e(a.N));
+        a.o_start = (int32_t)o; o = up16(o + 2 * up8e((int64_t)a.B + 1));
+        a.o_T = (int32_t)o; o = up16(o + 4 * (int64_t)a.B);
+        a.o_Q = (int32_t)o; o = up16(o + 8 * (int64_t)a.B);
+        a.o_acost = (int32_t)o; o = up16(o + 8 * ((int64_t)a.RG * (dv + 1) + a.RG));  // cost prefixes and totals
+        a.o_Jpre = (int32_t)o; o = up16(o + 8 * 144 * (int64_t)a.rv);  // J_pre, V_pre and their pivots
+        a.o_Jpiv = a.o_Jpre + 8 * 128 * a.rv;
+        int64_t tab = up16(4 * ((int64_t)a.G * a.D + 2 * a.G + a.D));
+        a.o_hcnt = (int32_t)tab; tab = up16(tab + 4 * (int64_t)a.RG);
+        a.o_hcell = (int32_t)tab; tab = up16(tab + 4 * (int64_t)a.RG * dv);
+        a.o_tshared = (int32_t)tab;
+        *shared_out = up16(tab + (cg ? 0 : 4 * (int64_t)a.N));
+        return o;
+    };
     const int64_t lim = 160 * 1024;
-    if (shared + member > lim) return false;
     int64_t want = ((int64_t)a.pop + n_cu - 1) / n_cu;
     want = want < 1 ? 1 : (want > kRunMaxWaves ? kRunMaxWaves : want);
-    const int64_t cap = (lim - shared) / member;
+    int64_t shared = 0, member = layout(false, &shared);
+    int64_t cap = shared + member <= lim ? (lim - shared) / member : 0;
+    a.cg = 0;
+    // ROUTEPACK_CHAIN_LAYOUT=hbm asks for the HBM layout (P = 32), =lds forbids it
+    const char *lay = getenv("ROUTEPACK_CHAIN_LAYOUT");
+    const bool force_hbm = lay && strcmp(lay, "hbm") == 0, no_hbm = lay && strcmp(lay, "lds") == 0;
+    if (force_hbm && P != 32) return false;
+    if (((cap < want && !no_hbm) || force_hbm) && P == 32) {
+        // the population cannot be resident at once: more members per CU
+        // with the cell array and the lengths in HBM (compiled for P = 32)
+        int64_t shared_g = 0;
+        const int64_t member_g = layout(true, &shared_g);
+        const int64_t cap_g = shared_g + member_g <= lim ? (lim - shared_g) / member_g : 0;
+        if (cap_g > cap || (force_hbm && cap_g >= 1)) {
+            a.cg = 1;
+            shared = shared_g;
+            member = member_g;
+            cap = cap_g;
+        } else {
+            layout(false, &shared);
+        }
+    }
+    if (cap < 1) return false;
     a.mpw = (int32_t)(want < cap ? want : cap);
     a.lds_shared = (int32_t)shared;
     a.lds_member = (int32_t)member;
@@ -1743,14 +1794,14 @@ bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out,
     return true;
 }
 
-template <int PV, int DV, int GV, int LV>
+template <int PV, int DV, int GV, int LV, bool CG>
 static int chain_launch_t(const AnnealArgs &a, hipStream_t stream) {
     const size_t lds = (size_t)a.lds_shared + (size_t)a.mpw * a.lds_member;
-    if (hipFuncSetAttribute((const void *)k_anneal_chain<PV, DV, GV, LV>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)lds) != hipSuccess)
+    if (hipFuncSetAttribute((const void *)k_anneal_chain<PV, DV, GV, LV, CG>,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
         return ROUTEPACK_E_DEVICE;
     const unsigned grid = (unsigned)((a.pop + a.mpw - 1) / a.mpw);
-    hipLaunchKernelGGL((k_anneal_chain<PV, DV, GV, LV>), dim3(grid), dim3(kWave * a.mpw), lds, stream, a);
+    hipLaunchKernelGGL((k_anneal_chain<PV, DV, GV, LV, CG>), dim3(grid), dim3(kWave * a.mpw), lds, stream, a);
     return hipGetLastError() == hipSuccess ? ROUTEPACK_OK : ROUTEPACK_E_DEVICE;
 }
 
@@ -1824,6 +1875,7 @@ static int chain_run_d(int v, const AnnealArgs &a, const RunArgs &r, int32_t pv,
 // kernel; ROUTEPACK_E_UNSUPPORTED when its workgroups cannot all be resident.
 int chain_run(const AnnealArgs &a, const RunArgs &r, int32_t pv, int32_t dv, int32_t n_cu, bool launch,
               hipStream_t stream) {
+    if (a.cg) return ROUTEPACK_E_UNSUPPORTED;  // (only the per-level kernel is compiled for it)
     const int v = chain_variant(a, r.step_log != nullptr);
     return dv == 8 ? chain_run_d<8>(v, a, r, pv, n_cu, launch, stream)
                    : chain_run_d<16>(v, a, r, pv, n_cu, launch, stream);
@@ -1831,12 +1883,16 @@ int chain_run(const AnnealArgs &a, const RunArgs &r, int32_t pv, int32_t dv, int
 
 template <int PV, int DV, int LV>
 static int chain_launch_v(int v, const AnnealArgs &a, hipStream_t stream) {
-    if (v == 2) {
-        if constexpr (PV == 32) return ROUTEPACK_E_UNSUPPORTED;  // (excluded by chain_plan)
-        else return chain_launch_t<PV, DV, 2, LV>(a, stream);
+    if constexpr (PV == 32) {
+        if (v == 2) return ROUTEPACK_E_UNSUPPORTED;  // (excluded by chain_plan)
+        if (a.cg) return v == 1 ? chain_launch_t<PV, DV, 1, LV, true>(a, stream)
+                                : chain_launch_t<PV, DV, 0, LV, true>(a, stream);
+    } else {
+        if (a.cg) return ROUTEPACK_E_UNSUPPORTED;  // (chain_plan takes it for P = 32 only)
+        if (v == 2) return chain_launch_t<PV, DV, 2, LV, false>(a, stream);
     }
-    if (v == 1) return chain_launch_t<PV, DV, 1, LV>(a, stream);
-    return chain_launch_t<PV, DV, 0, LV>(a, stream);
+    if (v == 1) return chain_launch_t<PV, DV, 1, LV, false>(a, stream);
+    return chain_launch_t<PV, DV, 0, LV, false>(a, stream);
 }
 
 template <int DV>

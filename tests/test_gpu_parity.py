@@ -255,13 +255,17 @@ MANY_LAYERS = {
 
 
 @gpu
-@pytest.mark.parametrize("kernel", KERNELS)
-@pytest.mark.parametrize("case", sorted(MANY_LAYERS))
+@pytest.mark.parametrize("case,kernel", [(c, k) for c in sorted(MANY_LAYERS) for k in KERNELS] +
+                         [(c, "chain_hbm") for c in sorted(MANY_LAYERS) if MANY_LAYERS[c]["ranks"] == 32])
 def test_anneal_many_layers(case, kernel, monkeypatch):
     """Full trajectories (12 levels of 256 proposals, population 32) on shapes
-    beyond 32 layers or 16 ranks, on every annealing kernel."""
+    beyond 32 layers or 16 ranks, on every annealing kernel; chain_hbm is the
+    per-level chain kernel with the cell array and lengths in HBM (32 ranks)."""
     import oracle as O
     rp = _rp()
+    if kernel == "chain_hbm":
+        monkeypatch.setenv("ROUTEPACK_CHAIN_LAYOUT", "hbm")
+        kernel = "chain"
     _use_kernel(monkeypatch, kernel)
     shape = dict(cap=4096, tmin=64, tmax=1500, pop=32, levels=12)
     shape.update(MANY_LAYERS[case])
