@@ -1,5 +1,7 @@
 /*
- * routepack_probe.h -- measurement aid shipped with the RoutePack library.
+ * routepack_probe.h -- measurement aid built beside the RoutePack library,
+ * as its own shared library (libroutepack_probe.so); libroutepack.so does
+ * not contain it.
  *
  * Not part of the method.  The annealing kernels keep each member's packing
  * state in LDS, so their roofline is quoted against the LDS read bandwidth

@@ -26,8 +26,10 @@ EXPORTS = ("routepack_aggregate_demand", "routepack_place_experts", "routepack_p
            "routepack_anneal", "routepack_eval_objective", "routepack_select_population",
            "routepack_row_lower_bound", "routepack_fixed_bin_search", "routepack_project_demand",
            "routepack_strerror")
-# measurement aid declared in include/routepack_probe.h (not part of the method)
+# measurement aid declared in include/routepack_probe.h (not part of the method),
+# built as its own library
 PROBE_EXPORTS = ("routepack_probe_lds_read",)
+PROBE_LIB_PATH = os.path.join(_HERE, "libroutepack_probe.so")
 
 
 class RoutepackError(RuntimeError):
@@ -76,8 +78,6 @@ def load_library():
         lib.routepack_row_lower_bound.argtypes = [P, vp, C.POINTER(C.c_int32), C.POINTER(C.c_int64), vp]
         lib.routepack_fixed_bin_search.argtypes = [P, vp, i32, i64, C.POINTER(C.c_int32), C.POINTER(C.c_int64), vp,
                                                    vp]
-        lib.routepack_probe_lds_read.argtypes = [i32, i32, vp, C.POINTER(C.c_double), C.POINTER(C.c_int64), vp]
-        lib.routepack_probe_lds_read.restype = C.c_int
         lib.routepack_strerror.argtypes = [C.c_int]
         lib.routepack_strerror.restype = C.c_char_p
         for f in EXPORTS:
@@ -273,11 +273,28 @@ def eval_objective(prob: Problem, lengths, q, n_rows, layouts, rank_load=None, w
     return dict(scores=sc, status=st, J=J, diag=dg)
 
 
+_probe_lib = None
+
+
+def load_probe_library():
+    """Loads libroutepack_probe.so (the LDS read-bandwidth probe)."""
+    global _probe_lib
+    if _probe_lib is None:
+        if not os.path.exists(PROBE_LIB_PATH):
+            raise RuntimeError(f"{PROBE_LIB_PATH} is missing: run __graft_entry__.build() first")
+        lib = C.CDLL(PROBE_LIB_PATH)
+        lib.routepack_probe_lds_read.argtypes = [C.c_int32, C.c_int32, C.c_void_p, C.POINTER(C.c_double),
+                                                 C.POINTER(C.c_int64), C.c_void_p]
+        lib.routepack_probe_lds_read.restype = C.c_int
+        _probe_lib = lib
+    return _probe_lib
+
+
 def probe_lds_read(n_workgroups=2048, reps=8192):
     """LDS read bandwidth of this device (routepack_probe_lds_read): returns
     (bytes read, launch ms).  A measurement aid, not part of the method."""
     torch = _torch()
-    lib = load_library()
+    lib = load_probe_library()
     sink = torch.empty(n_workgroups * 256, dtype=torch.int32, device="cuda")
     ms, nbytes = C.c_double(0.0), C.c_int64(0)
     _check("routepack_probe_lds_read",

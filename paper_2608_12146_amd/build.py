@@ -1,7 +1,9 @@
-"""Builds the HIP library libroutepack.so for gfx950 with hipcc (in-tree).
+"""Builds the HIP library libroutepack.so for gfx950 with hipcc (in-tree),
+and the measurement aid libroutepack_probe.so (the LDS read-bandwidth probe,
+not part of the method) from rp_probe.hip.
 
 Each source compiles to its own object in parallel (no device code crosses a
-translation unit), then one hipcc line links the shared library."""
+translation unit), then one hipcc line links each shared library."""
 from __future__ import annotations
 
 import glob
@@ -12,6 +14,8 @@ from concurrent.futures import ThreadPoolExecutor
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libroutepack.so")
+PROBE_LIB = os.path.join(HERE, "libroutepack_probe.so")
+PROBE_SOURCE = "rp_probe.hip"
 OBJ_DIR = os.path.join(ROOT, "_build", "obj")
 
 HIPCC_FLAGS = [
@@ -26,7 +30,8 @@ HIPCC_FLAGS = [
 
 
 def sources():
-    return sorted(glob.glob(os.path.join(HERE, "csrc", "*.hip")))
+    """The library's sources (every .hip file but the probe's)."""
+    return sorted(f for f in glob.glob(os.path.join(HERE, "csrc", "*.hip")) if os.path.basename(f) != PROBE_SOURCE)
 
 
 def _jobs() -> int:
@@ -53,20 +58,22 @@ def build(verbose: bool = False) -> str:
         return obj
 
     with ThreadPoolExecutor(_jobs()) as ex:
-        objs = list(ex.map(compile_one, sources()))
-    tmp = LIB + f".tmp{tag}"
-    cmd = [hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
-    if verbose:
-        print(" ".join(cmd), flush=True)
+        objs = list(ex.map(compile_one, sources() + [os.path.join(HERE, "csrc", PROBE_SOURCE)]))
+    probe_obj = objs.pop()
     try:
-        subprocess.check_call(cmd)
+        for target, parts in ((LIB, objs), (PROBE_LIB, [probe_obj])):
+            tmp = target + f".tmp{tag}"
+            cmd = [hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", *parts, "-o", tmp]
+            if verbose:
+                print(" ".join(cmd), flush=True)
+            subprocess.check_call(cmd)
+            os.replace(tmp, target)
     finally:
-        for o in objs:
+        for o in objs + [probe_obj]:
             try:
                 os.remove(o)
             except OSError:
                 pass
-    os.replace(tmp, LIB)
     return LIB
 
 

@@ -600,7 +600,7 @@ def test_lds_probe_reads_what_it_claims():
 
     import torch
     rp = _rp()
-    lib = rp.load_library()
+    lib = rp.load_probe_library()
     nwg, reps = 3, 4099          # reps not a multiple of the 16-step period
     sink = torch.zeros(nwg * 256, dtype=torch.int32, device="cuda")
     ms, nb = C.c_double(0.0), C.c_int64(0)
