@@ -808,8 +808,13 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
             const int32_t ha = ra * G + ga, hb = rb * G + gb;
             const bool two = ha != hb;
             // W rows of a and b, q rows of i and j: issue the loads first.
+            // They are issued (and consumed below) on every path, also when
+            // both cells are in one row-shard (the row is then read twice):
+            // a load left pending on some path would make the compiler wait
+            // on the memory counter, which the previous commit's W stores
+            // share, before the next move's loads.
             int4 wr[LV * PV / 4], qx[LV * PV / 4], qy[LV * PV / 4];
-            if (two) load_rows(i, j, ha, hb, wr, qx, qy);
+            load_rows(i, j, ha, hb, wr, qx, qy);
             // Cell statistics of the two row-shards (lanes (half, cx)) and the
             // commit inputs, read in one stage while the row loads are in
             // flight: the member ranges of both cells and, when both fit 32
@@ -868,14 +873,14 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
             const int64_t Jhb = row_entry<RV>(Jr, Jr2, hb);
             int64_t Ja, Jb;
             int32_t nw[LV * PV];
-            if (two) {
 #pragma unroll
-                for (int x = 0; x < LV * PV / 4; ++x) {
-                    nw[4 * x + 0] = wr[x].x - qx[x].x + qy[x].x;
-                    nw[4 * x + 1] = wr[x].y - qx[x].y + qy[x].y;
-                    nw[4 * x + 2] = wr[x].z - qx[x].z + qy[x].z;
-                    nw[4 * x + 3] = wr[x].w - qx[x].w + qy[x].w;
-                }
+            for (int x = 0; x < LV * PV / 4; ++x) {
+                nw[4 * x + 0] = wr[x].x - qx[x].x + qy[x].x;
+                nw[4 * x + 1] = wr[x].y - qx[x].y + qy[x].y;
+                nw[4 * x + 2] = wr[x].z - qx[x].z + qy[x].z;
+                nw[4 * x + 3] = wr[x].w - qx[x].w + qy[x].w;
+            }
+            if (two) {
                 // the lane's share of the layer sum: the rank maximum of each
                 // of its layers (at most L W_b < 2^31 in the 32-bit case)
                 int32_t mx32 = 0;
