@@ -1,5 +1,6 @@
 // Validation, scratch, window bounds and status strings for the RoutePack
 // C-ABI library.
+#include <atomic>
 #include <math.h>
 #include <string.h>
 
@@ -36,6 +37,23 @@ int check_problem(const routepack_problem *p, Topology *topo) {
     if (topo) *topo = t;
     return ROUTEPACK_OK;
 }
+
+// The device's default stream-ordered pool keeps the memory freed into it
+// (release threshold: unlimited), set once per device: otherwise every
+// synchronisation hands the pool's memory back and the next call maps it
+// again, which costs milliseconds for the annealing state.
+static void keep_pool_memory() {
+    static std::atomic<uint64_t> done{0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return;
+    if (done.fetch_or(1ull << dev) & (1ull << dev)) return;
+    hipMemPool_t pool = nullptr;
+    if (hipDeviceGetDefaultMemPool(&pool, dev) != hipSuccess || !pool) return;
+    uint64_t threshold = UINT64_MAX;
+    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &threshold);
+}
+
+Scratch::Scratch(hipStream_t s) : stream_(s) { keep_pool_memory(); }
 
 Scratch::~Scratch() {
     for (void *q : ptrs_) (void)hipFreeAsync(q, stream_);

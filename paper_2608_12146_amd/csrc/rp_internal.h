@@ -38,7 +38,7 @@ int check_problem(const routepack_problem *p, Topology *topo);
 // RAII device scratch allocated stream-ordered on one stream.
 class Scratch {
   public:
-    explicit Scratch(hipStream_t s) : stream_(s) {}
+    explicit Scratch(hipStream_t s);
     ~Scratch();
     // Allocates n bytes (256-byte aligned); returns nullptr on failure.
     void *alloc(size_t n);
