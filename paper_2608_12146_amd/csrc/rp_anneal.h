@@ -88,7 +88,12 @@ struct RunArgs {
     unsigned *pub;         // [pop] per slab: the last level whose image it published (zero at launch)
     unsigned *got;         // [pop] per slab: receivers that have copied its image (zero at launch)
     unsigned spin_limit;   // polls before a barrier or hand-over wait gives up (sets err)
+    const uint32_t *vwords;  // [n_sweeps] resampling offset word V of each level (tag-2 Philox block)
 };
+
+// V of levels offset .. offset + n - 1 into v (the run kernel reads them at
+// each level end instead of drawing the Philox block there).
+int launch_resample_words(uint64_t seed, int32_t offset, int32_t n, uint32_t *v, hipStream_t stream);
 
 // Bytes of the whole-schedule kernel's level-end tables for a population.
 int64_t run_lend_bytes(int32_t pop);

@@ -1187,6 +1187,7 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
     if (whole) {
         // The whole schedule in one cooperative launch.
         double *temps_d = scr.get<double>(prm->n_sweeps);
+        uint32_t *vwords = scr.get<uint32_t>(prm->n_sweeps);
         unsigned *bar = scr.get<unsigned>(2);
         int32_t *slab_final = scr.get<int32_t>(pop_size);
         // by level parity: a workgroup that runs ahead into the next level
@@ -1202,6 +1203,8 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
                               stream));
         RP_HIP(hipMemsetAsync(bar, 0, 2 * sizeof(unsigned), stream));
         RP_HIP(hipMemsetAsync(flags, 0, 2 * sizeof(unsigned) * (size_t)pop_size, stream));
+        RP_TRY(launch_resample_words(a.seed, prm->sweep_offset, prm->n_sweeps, vwords, stream));
+        run.vwords = vwords;
         a.slabs = slabA;
         a.xscore = best_score;
         run.temps = temps_d;

@@ -1270,12 +1270,28 @@ __device__ inline void member_receive(const AnnealArgs &a, char *mine, const cha
     wsync();
 }
 
+// Stores and loads at device scope (every XCD): the store writes through to
+// memory and the load reads from there, so data passed this way between
+// workgroups needs no L2 writeback or invalidation around a barrier.
+__device__ inline void st_dev(void *p, uint64_t v) {
+    __hip_atomic_store(reinterpret_cast<uint64_t *>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline uint64_t ld_dev(const void *p) {
+    return __hip_atomic_load(reinterpret_cast<const uint64_t *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Grid-wide barrier on a monotonic arrival counter; false if it timed out
 // (then every workgroup stops).  Every thread of the workgroup takes part.
+// FULL: release and acquire at agent scope (the XCD's L2 written back, then
+// invalidated), so ordinary stores before it are visible to ordinary loads
+// after it in every workgroup.  Otherwise only device-scope stores (st_dev)
+// made before it are visible after it, to device-scope loads (ld_dev).
+template <bool FULL>
 __device__ inline bool grid_sync(unsigned *bar, unsigned target, int32_t *err, unsigned spin_limit, int32_t *s_ok) {
+    if (!FULL) __builtin_amdgcn_s_waitcnt(0);  // this wave's st_dev stores have completed
     __syncthreads();
     if (threadIdx.x == 0) {
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        if (FULL) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
         __hip_atomic_fetch_add(bar, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         unsigned spins = 0;
         int32_t good = 1;
@@ -1289,7 +1305,7 @@ __device__ inline bool grid_sync(unsigned *bar, unsigned target, int32_t *err, u
                 break;
             }
         }
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        if (FULL) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         *s_ok = good;
     }
     __syncthreads();
@@ -1449,7 +1465,7 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
                 a, M, tb, g.W, m, level, temp, s_xs[0], s_xs[1], s_xs[2],
                 r.step_log ? r.step_log + ((int64_t)n * pop + m) * K : nullptr, a.results + (int64_t)m * kRes,
                 r.trace ? r.trace + ((int64_t)n * pop + m) * 8 : nullptr, R);
-            if (lane == 0) r.energy[(int64_t)(n & 1) * pop + m] = lo.e;
+            if (lane == 0) st_dev(r.energy + (int64_t)(n & 1) * pop + m, __builtin_bit_cast(uint64_t, lo.e));
             k0 = lo.b0;
             k1 = lo.b1;
             k2 = lo.b2;
@@ -1469,10 +1485,13 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
                     for (int f = 0; f < 4; ++f) s_k[0][f] = s_k[w][f];
                 s_dred[0] = s_dred[w] < s_dred[0] ? s_dred[w] : s_dred[0];
             }
-            for (int f = 0; f < 4; ++f) r.wg_best[((int64_t)(n & 1) * nb + blockIdx.x) * 4 + f] = s_k[0][f];
-            r.wg_emin[(n & 1) * nb + blockIdx.x] = s_dred[0];
+            for (int f = 0; f < 4; ++f)
+                st_dev(r.wg_best + ((int64_t)(n & 1) * nb + blockIdx.x) * 4 + f, (uint64_t)s_k[0][f]);
+            st_dev(r.wg_emin + (n & 1) * nb + blockIdx.x, __builtin_bit_cast(uint64_t, s_dred[0]));
         }
-        if (!grid_sync(r.bar, (unsigned)nb * ++epoch, r.err, r.spin_limit, &s_ok)) return;  // A
+        // (the level's results cross workgroups by device-scope stores and
+        // loads only: no L2 writeback here)
+        if (!grid_sync<false>(r.bar, (unsigned)nb * ++epoch, r.err, r.spin_limit, &s_ok)) return;  // A
 
         // ---- every workgroup: incumbent and minimum energy from the workgroup summaries
         const double t_next = n + 1 < r.n_sweeps ? r.temps[n + 1] : r.t_after;
@@ -1484,8 +1503,9 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
             emin = __builtin_inf();
             for (int b = tid; b < nb; b += nt) {
                 const int64_t *wb = r.wg_best + ((int64_t)(n & 1) * nb + b) * 4;
-                const int64_t v0 = wb[0], v1 = wb[1], v2 = wb[2], vj = wb[3];
-                const double e = r.wg_emin[(n & 1) * nb + b];
+                const int64_t v0 = (int64_t)ld_dev(wb), v1 = (int64_t)ld_dev(wb + 1), v2 = (int64_t)ld_dev(wb + 2),
+                              vj = (int64_t)ld_dev(wb + 3);
+                const double e = __builtin_bit_cast(double, ld_dev(r.wg_emin + (n & 1) * nb + b));
                 if (lex_less(v0, v1, v2, k0, k1, k2) || (v0 == k0 && v1 == k1 && v2 == k2 && vj < kj)) {
                     k0 = v0; k1 = v1; k2 = v2; kj = vj;
                 }
@@ -1498,7 +1518,7 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
                 s_dred[wv] = emin;
             }
             // the energies of this thread's members (used by the resampling weights)
-            for (int32_t j = jlo; j < jhi; ++j) Fs[j] = __builtin_bit_cast(uint64_t, r.energy[(int64_t)(n & 1) * pop + j]);
+            for (int32_t j = jlo; j < jhi; ++j) Fs[j] = ld_dev(r.energy + (int64_t)(n & 1) * pop + j);
             __syncthreads();
             if (tid == 0) {
                 for (int w = 1; w < nwv; ++w) {
@@ -1518,7 +1538,12 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
             }
             __syncthreads();
         }
-        if (s_win >= 0) {
+        // A level that moved the incumbent reads rows that members wrote
+        // with ordinary stores (the winner's trajectory best here, the
+        // parents' W rows below): a full barrier first.
+        const bool sync_b = s_win >= 0;
+        if (sync_b && !grid_sync<true>(r.bar, (unsigned)nb * ++epoch, r.err, r.spin_limit, &s_ok)) return;
+        if (sync_b) {
             // x* := the winner's trajectory best, one slice per workgroup
             const int32_t sl = (N + nb - 1) / nb, x0 = blockIdx.x * sl, x1 = x0 + sl < N ? x0 + sl : N;
             const int32_t *src = a.best + (int64_t)s_win * N;
@@ -1544,8 +1569,7 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
                 Fs[j] = run;
             }
             __syncthreads();
-            const U64x4 blk = philox4x64_10(0, (uint64_t)(uint32_t)level, 0xFFFFFFFFull, 2, a.seed, 0);
-            const uint64_t V = blk.v[0] >> 32;
+            const uint64_t V = r.vwords[n];
             // children of this thread: [jlo, jhi); parents are non-decreasing
             int32_t pj = jlo < pop ? jlo : pop - 1;
             for (int32_t mm = jlo; mm < jhi; ++mm) {
@@ -1573,7 +1597,6 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
         // parent's slab, waits for that count before its next level changes
         // W.  s_win is the same in every workgroup, so all of them take the
         // same path.
-        const bool sync_b = s_win >= 0;
         const unsigned token = (unsigned)n + 1;  // (flags are zero at launch)
         int32_t m_next = m, src_slab = -1, n_recv = 0;
         bool publish = false;
@@ -1656,7 +1679,7 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
                 }
             }
         }
-        if (sync_b && !grid_sync(r.bar, (unsigned)nb * ++epoch, r.err, r.spin_limit, &s_ok)) return;  // B
+        if (sync_b && !grid_sync<true>(r.bar, (unsigned)nb * ++epoch, r.err, r.spin_limit, &s_ok)) return;  // B
         if (resample) {
             for (int32_t mm = tid; mm < pop; mm += nt) slab[mm] = slabn[mm];
             __syncthreads();
@@ -1688,6 +1711,22 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
     if (active) member_store<GV == 2 ? 2 : 1>(a, M, g, R);
     if (blockIdx.x == 0)
         for (int32_t mm = tid; mm < pop; mm += nt) r.slab_of_out[mm] = slab[mm];
+}
+
+// Resampling offset words (Alg. 3 reweighting step): V of a level is the
+// high half of the first word of the tag-2 Philox block with counter
+// (0, level, 2^32 - 1, 2); one thread per level.
+__global__ void __launch_bounds__(256) k_resample_words(uint64_t seed, int32_t offset, int32_t n, uint32_t *v) {
+    const int32_t x = blockIdx.x * blockDim.x + threadIdx.x;
+    if (x >= n) return;
+    const U64x4 blk = philox4x64_10(0, (uint64_t)(uint32_t)(offset + x), 0xFFFFFFFFull, 2, seed, 0);
+    v[x] = (uint32_t)(blk.v[0] >> 32);
+}
+
+int launch_resample_words(uint64_t seed, int32_t offset, int32_t n, uint32_t *v, hipStream_t stream) {
+    if (n <= 0) return ROUTEPACK_OK;
+    hipLaunchKernelGGL(k_resample_words, dim3((n + 255) / 256), dim3(256), 0, stream, seed, offset, n, v);
+    return hipGetLastError() == hipSuccess ? ROUTEPACK_OK : ROUTEPACK_E_DEVICE;
 }
 
 // Rows of L x P int32 from layer-major [L][P] to chunk-major [P/4][L][4],
