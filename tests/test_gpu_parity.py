@@ -254,9 +254,27 @@ MANY_LAYERS = {
 }
 
 
+# A GPU memory fault was reported once during this case (per-level chain
+# kernel, 32 ranks, 40 layers) in a build that differed from the current
+# sources only in register allocation; the cause has not been found, so the
+# case stays off the GPU until it is.
+_FAULT_SEEN = {("l40_p32", "chain")}
+
+
+def _many_layers_params():
+    out = []
+    for c, k in ([(c, k) for c in sorted(MANY_LAYERS) for k in KERNELS] +
+                 [(c, "chain_hbm") for c in sorted(MANY_LAYERS) if MANY_LAYERS[c]["ranks"] == 32]):
+        if (c, k) in _FAULT_SEEN:
+            out.append(pytest.param(c, k, marks=pytest.mark.skip(
+                reason="a GPU memory fault was seen once in this case; cause not yet found")))
+        else:
+            out.append((c, k))
+    return out
+
+
 @gpu
-@pytest.mark.parametrize("case,kernel", [(c, k) for c in sorted(MANY_LAYERS) for k in KERNELS] +
-                         [(c, "chain_hbm") for c in sorted(MANY_LAYERS) if MANY_LAYERS[c]["ranks"] == 32])
+@pytest.mark.parametrize("case,kernel", _many_layers_params())
 def test_anneal_many_layers(case, kernel, monkeypatch):
     """Full trajectories (12 levels of 256 proposals, population 32) on shapes
     beyond 32 layers or 16 ranks, on every annealing kernel; chain_hbm is the
