@@ -185,13 +185,14 @@ typedef struct routepack_anneal_params {
  *              run in the same kernel): CHAIN shapes whose workgroups can
  *              all be resident at once
  *   CHAIN      one wave per member, lanes over (row-shard, layer) and cells:
- *              P in {4, 8, 16, 32}, L <= 32 (L <= 64 when P >= 16), R G <= 128
- *              (<= 64 when P = 32), <= 16 slots per shard, N < 65536.  When
- *              the population cannot be resident at once and P = 32, the
- *              per-level launch may keep each member's cell array and the
- *              lengths in HBM to fit more members per CU
- *              (ROUTEPACK_CHAIN_LAYOUT=hbm asks for that layout, =lds
- *              forbids it)
+ *              P in {4, 8, 16, 32, 64}, L <= 32 (L <= 64 when P >= 16),
+ *              R G <= 128 (<= 64 when P >= 32), <= 16 slots per shard (<= 32
+ *              when P = 64), N < 65536.  When the population cannot be
+ *              resident at once and P = 32, the per-level launch may keep
+ *              each member's cell array and the lengths in HBM to fit more
+ *              members per CU (ROUTEPACK_CHAIN_LAYOUT=hbm asks for that
+ *              layout, =lds forbids it); P = 64 always runs that layout (a
+ *              64-rank row is formed 16 ranks at a time), per level only
  *   WAVE       one wave per member, lanes over flat 64-entry strides:
  *              R G <= 512, member state within LDS
  *   WORKGROUP  one workgroup per member, state in HBM: every problem within

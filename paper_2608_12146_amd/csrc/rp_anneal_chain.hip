@@ -40,20 +40,28 @@ __device__ inline void wsync() {
 }
 
 // Inclusive prefix sum over the first W lanes (W = 8 or 16) of each 16-lane
-// row.
+// row; W = 32: over each 32-lane half (rows 1 and 3 add the last lane of
+// rows 0 and 2).
 template <int W>
 __device__ inline int64_t row_incl_scan64(int64_t v) {
     v += dpp64<kDppRowShr1>(v, 0);
     v += dpp64<kDppRowShr1 + 1>(v, 0);
     v += dpp64<kDppRowShr1 + 3>(v, 0);
     if (W > 8) v += dpp64<kDppRowShr1 + 7>(v, 0);
+    if (W > 16) v += dpp64<kDppRowBcast15, 0xA>(v, 0);
     return v;
 }
 
 // Maximum over the first W lanes (W = 8 or 16) of each 16-lane row, held by
-// those lanes.
+// those lanes; W = 32: over each 32-lane half, held by the lanes of rows 1
+// and 3 (lanes 16 and 48 among them).
 template <int W>
 __device__ inline int64_t row_head_max64(int64_t v) {
+    if (W > 16) {
+        v = row_max64(v);
+        const int64_t o = dpp64<kDppRowBcast15, 0xA>(v, v);
+        return o > v ? o : v;
+    }
     if (W > 8) return row_max64(v);
     int64_t o;
     o = dpp64<kDppXor1>(v, v); v = o > v ? o : v;
@@ -730,8 +738,11 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
     }
     int64_t n_acc = 0, n_eval = 0;
     double e_cur = GV == 1 ? energy_pow2(a, s0, s1, s2) : energy_k(a, s0, s1, s2);
-    const int half = lane >> 5, hl = lane & 31, cx = lane & 15;
-    const bool cell_lane = (lane & 16) == 0;
+    const int half = lane >> 5, hl = lane & 31;
+    // cells of a row-shard: lane (half, x) holds its x-th slot, x < 16 (all
+    // 32 lanes of the half with up to 32 slots)
+    const int cx = DV > 16 ? hl : (lane & 15);
+    const bool cell_lane = DV > 16 || (lane & 16) == 0;
     // layer v of the lane is hl + 32 v (v < LV), held when below L
     auto lay_act = [&](int v) { return hl + 32 * v < L; };
     // Loads of one move: lane (half, hl) reads its layers of row-shard ha
@@ -755,6 +766,42 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                 qx[v * (PV / 4) + x] = xp[x * L];
                 qy[v * (PV / 4) + x] = yp[x * L];
             }
+        }
+    };
+
+    // 64 ranks: a lane's new row (128 entries with two layers) is formed
+    // from the W row and the two q rows 16 ranks at a time, so only one
+    // chunk of each is in registers besides the new row.
+    auto rows_nw64 = [&](int32_t i, int32_t j, int32_t ha, int32_t hb, int32_t *nw) {
+        const int32_t row = half ? hb : ha;
+        const int32_t *qi = a.qt + (int64_t)i * a.LP, *qj = j >= 0 ? a.qt + (int64_t)j * a.LP : a.qzero;
+        constexpr int CH = 4;  // 16-byte chunks (four ranks each) per pass
+#pragma unroll
+        for (int c = 0; c < PV / 4; c += CH) {
+            int4 w4[LV * CH], x4[LV * CH], y4[LV * CH];
+#pragma unroll
+            for (int v = 0; v < LV; ++v) {
+                const int32_t ll = lay_act(v) ? hl + 32 * v : L - 1;
+                const int4 *wp = reinterpret_cast<const int4 *>(W + (int64_t)row * a.LP) + ll;
+                const int4 *xp = reinterpret_cast<const int4 *>(half ? qj : qi) + ll;
+                const int4 *yp = reinterpret_cast<const int4 *>(half ? qi : qj) + ll;
+#pragma unroll
+                for (int x = 0; x < CH; ++x) {
+                    w4[v * CH + x] = wp[(c + x) * L];
+                    x4[v * CH + x] = xp[(c + x) * L];
+                    y4[v * CH + x] = yp[(c + x) * L];
+                }
+            }
+#pragma unroll
+            for (int v = 0; v < LV; ++v)
+#pragma unroll
+                for (int x = 0; x < CH; ++x) {
+                    const int y = v * PV + 4 * (c + x), u = v * CH + x;
+                    nw[y + 0] = w4[u].x - x4[u].x + y4[u].x;
+                    nw[y + 1] = w4[u].y - x4[u].y + y4[u].y;
+                    nw[y + 2] = w4[u].z - x4[u].z + y4[u].z;
+                    nw[y + 3] = w4[u].w - x4[u].w + y4[u].w;
+                }
         }
     };
 
@@ -813,8 +860,9 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
             // a load left pending on some path would make the compiler wait
             // on the memory counter, which the previous commit's W stores
             // share, before the next move's loads.
-            int4 wr[LV * PV / 4], qx[LV * PV / 4], qy[LV * PV / 4];
-            load_rows(i, j, ha, hb, wr, qx, qy);
+            constexpr int NR = PV <= 32 ? LV * PV / 4 : 1;  // (64 ranks: rows_nw64 below)
+            int4 wr[NR], qx[NR], qy[NR];
+            if constexpr (PV <= 32) load_rows(i, j, ha, hb, wr, qx, qy);
             // Cell statistics of the two row-shards (lanes (half, cx)) and the
             // commit inputs, read in one stage while the row loads are in
             // flight: the member ranges of both cells and, when both fit 32
@@ -867,18 +915,22 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                     Arow = (int64_t)((uint64_t)Arow + (uint64_t)row_head_max64<DV>(cact ? cost : LLONG_MIN));
                 }
             }
-            const int64_t Aa = (int64_t)readlane64((uint64_t)Arow, 0);
-            const int64_t Ab = two ? (int64_t)readlane64((uint64_t)Arow, 32) : Aa;
+            const int64_t Aa = (int64_t)readlane64((uint64_t)Arow, DV > 16 ? 16 : 0);
+            const int64_t Ab = two ? (int64_t)readlane64((uint64_t)Arow, DV > 16 ? 48 : 32) : Aa;
             const int64_t Jha = row_entry<RV>(Jr, Jr2, ha), Aha = row_entry<RV>(Ar, Ar2, ha);
             const int64_t Jhb = row_entry<RV>(Jr, Jr2, hb);
             int64_t Ja, Jb;
             int32_t nw[LV * PV];
+            if constexpr (PV <= 32) {
 #pragma unroll
-            for (int x = 0; x < LV * PV / 4; ++x) {
-                nw[4 * x + 0] = wr[x].x - qx[x].x + qy[x].x;
-                nw[4 * x + 1] = wr[x].y - qx[x].y + qy[x].y;
-                nw[4 * x + 2] = wr[x].z - qx[x].z + qy[x].z;
-                nw[4 * x + 3] = wr[x].w - qx[x].w + qy[x].w;
+                for (int x = 0; x < LV * PV / 4; ++x) {
+                    nw[4 * x + 0] = wr[x].x - qx[x].x + qy[x].x;
+                    nw[4 * x + 1] = wr[x].y - qx[x].y + qy[x].y;
+                    nw[4 * x + 2] = wr[x].z - qx[x].z + qy[x].z;
+                    nw[4 * x + 3] = wr[x].w - qx[x].w + qy[x].w;
+                }
+            } else {
+                rows_nw64(i, j, ha, hb, nw);
             }
             if (two) {
                 // the lane's share of the layer sum: the rank maximum of each
@@ -1734,7 +1786,7 @@ int launch_resample_words(uint64_t seed, int32_t offset, int32_t n, uint32_t *v,
 __global__ void __launch_bounds__(256) k_rows_to_chunks(const int32_t *src, int32_t *dst, int64_t n_rows,
                                                       int64_t row_stride, int64_t rows_per_group,
                                                       int64_t group_stride, int32_t L, int32_t P) {
-    __shared__ int32_t row[2048];  // L * P <= 64 * 32
+    __shared__ int32_t row[4096];  // L * P <= 64 * 64
     const int64_t rr = blockIdx.x;
     if (rr >= n_rows) return;
     const int64_t off = (rr / rows_per_group) * group_stride + (rr % rows_per_group) * row_stride;
@@ -1748,7 +1800,7 @@ __global__ void __launch_bounds__(256) k_rows_to_chunks(const int32_t *src, int3
 }
 
 int chain_prepare(AnnealArgs &a, int32_t *qt, hipStream_t stream) {
-    if (a.L * a.P > 2048 || (a.P & 3) != 0) return ROUTEPACK_E_UNSUPPORTED;
+    if (a.L * a.P > 4096 || (a.P & 3) != 0) return ROUTEPACK_E_UNSUPPORTED;
     if (a.LP > 0) {
         hipLaunchKernelGGL(k_rows_to_chunks, dim3((unsigned)a.N), dim3(256), 0, stream, a.q, qt, (int64_t)a.N,
                            (int64_t)a.LP, (int64_t)1, (int64_t)a.LP, a.L, a.P);
@@ -1766,17 +1818,19 @@ int chain_prepare(AnnealArgs &a, int32_t *qt, hipStream_t stream) {
 // shape (the caller then uses the flat wave kernel).
 bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out, int32_t *dv_out) {
     const int32_t P = a.P;
-    if (!(P == 4 || P == 8 || P == 16 || P == 32)) return false;
+    if (!(P == 4 || P == 8 || P == 16 || P == 32 || P == 64)) return false;
     // (L >= 1: each move loads its rows with a layer on every lane of a half;
-    // 33 to 64 layers take two layers per lane, compiled for P >= 16)
-    if (a.L < 1 || a.L > 64 || (a.L > 32 && P < 16) || a.RG > 2 * kWave || max_count > 16 || a.N > 65535 ||
-        a.B + 1 > 65535 || a.C > 2147483647LL)
+    // 33 to 64 layers take two layers per lane, compiled for P >= 16; up to
+    // 16 slots per row-shard, or 32 with 64 ranks)
+    if (a.L < 1 || a.L > 64 || (a.L > 32 && P < 16) || a.RG > 2 * kWave || max_count > (P == 64 ? 32 : 16) ||
+        a.N > 65535 || a.B + 1 > 65535 || a.C > 2147483647LL)
         return false;
-    // (32 ranks with two row-shards per lane are not compiled)
-    if (P == 32 && a.RG > kWave) return false;
+    // (32 or 64 ranks with two row-shards per lane are not compiled)
+    if (P >= 32 && a.RG > kWave) return false;
     a.lv = a.L > 32 ? 2 : 1;
     a.rv = a.RG > kWave ? 2 : 1;  // row-shards per lane
-    const int32_t dv = max_count <= 8 ? 8 : 16;
+    // (64 ranks are compiled with 32 slot lanes and the HBM layout only)
+    const int32_t dv = P == 64 ? 32 : (max_count <= 8 ? 8 : 16);
     a.dv = dv;
     a.ginv = (uint32_t)((((uint64_t)1 << 32) + (uint64_t)a.G - 1) / (uint64_t)a.G);
     a.dinv = (uint32_t)((((uint64_t)1 << 32) + (uint64_t)a.D - 1) / (uint64_t)a.D);
@@ -1813,14 +1867,16 @@ bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out,
     // ROUTEPACK_CHAIN_LAYOUT=hbm asks for the HBM layout (P = 32), =lds forbids it
     const char *lay = getenv("ROUTEPACK_CHAIN_LAYOUT");
     const bool force_hbm = lay && strcmp(lay, "hbm") == 0, no_hbm = lay && strcmp(lay, "lds") == 0;
-    if (force_hbm && P != 32) return false;
-    if (((cap < want && !no_hbm) || force_hbm) && P == 32) {
-        // the population cannot be resident at once: more members per CU
-        // with the cell array and the lengths in HBM (compiled for P = 32)
+    if (force_hbm && P < 32) return false;
+    if (P == 64 && no_hbm) return false;
+    if (((cap < want && !no_hbm) || force_hbm || P == 64) && P >= 32) {
+        // the population cannot be resident at once (or 64 ranks): more
+        // members per CU with the cell array and the lengths in HBM
+        // (compiled for P = 32 and 64)
         int64_t shared_g = 0;
         const int64_t member_g = layout(true, &shared_g);
         const int64_t cap_g = shared_g + member_g <= lim ? (lim - shared_g) / member_g : 0;
-        if (cap_g > cap || (force_hbm && cap_g >= 1)) {
+        if (cap_g > cap || ((force_hbm || P == 64) && cap_g >= 1)) {
             a.cg = 1;
             shared = shared_g;
             member = member_g;
@@ -1829,7 +1885,7 @@ bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out,
             layout(false, &shared);
         }
     }
-    if (cap < 1) return false;
+    if (cap < 1 || (P == 64 && !a.cg)) return false;
     a.mpw = (int32_t)(want < cap ? want : cap);
     a.lds_shared = (int32_t)shared;
     a.lds_member = (int32_t)member;
@@ -1919,7 +1975,8 @@ static int chain_run_d(int v, const AnnealArgs &a, const RunArgs &r, int32_t pv,
 // kernel; ROUTEPACK_E_UNSUPPORTED when its workgroups cannot all be resident.
 int chain_run(const AnnealArgs &a, const RunArgs &r, int32_t pv, int32_t dv, int32_t n_cu, bool launch,
               hipStream_t stream) {
-    if (a.cg) return ROUTEPACK_E_UNSUPPORTED;  // (only the per-level kernel is compiled for it)
+    // (only the per-level kernel is compiled for the HBM layout and 64 ranks)
+    if (a.cg || dv == 32) return ROUTEPACK_E_UNSUPPORTED;
     const int v = chain_variant(a, r.step_log != nullptr);
     return dv == 8 ? chain_run_d<8>(v, a, r, pv, n_cu, launch, stream)
                    : chain_run_d<16>(v, a, r, pv, n_cu, launch, stream);
@@ -1927,16 +1984,20 @@ int chain_run(const AnnealArgs &a, const RunArgs &r, int32_t pv, int32_t dv, int
 
 template <int PV, int DV, int LV>
 static int chain_launch_v(int v, const AnnealArgs &a, hipStream_t stream) {
-    if constexpr (PV == 32) {
+    if constexpr (PV >= 32) {
         if (v == 2) return ROUTEPACK_E_UNSUPPORTED;  // (excluded by chain_plan)
         if (a.cg) return v == 1 ? chain_launch_t<PV, DV, 1, LV, true>(a, stream)
                                 : chain_launch_t<PV, DV, 0, LV, true>(a, stream);
     } else {
-        if (a.cg) return ROUTEPACK_E_UNSUPPORTED;  // (chain_plan takes it for P = 32 only)
+        if (a.cg) return ROUTEPACK_E_UNSUPPORTED;  // (chain_plan takes it for P = 32 and 64 only)
         if (v == 2) return chain_launch_t<PV, DV, 2, LV, false>(a, stream);
     }
-    if (v == 1) return chain_launch_t<PV, DV, 1, LV, false>(a, stream);
-    return chain_launch_t<PV, DV, 0, LV, false>(a, stream);
+    if constexpr (PV == 64) {
+        return ROUTEPACK_E_UNSUPPORTED;  // (64 ranks: the HBM layout only)
+    } else {
+        if (v == 1) return chain_launch_t<PV, DV, 1, LV, false>(a, stream);
+        return chain_launch_t<PV, DV, 0, LV, false>(a, stream);
+    }
 }
 
 template <int DV>
@@ -1959,6 +2020,10 @@ static int chain_launch_d(int v, const AnnealArgs &a, int32_t pv, hipStream_t st
 
 int launch_anneal_chain(const AnnealArgs &a, int32_t pv, int32_t dv, hipStream_t stream) {
     const int v = chain_variant(a, a.step_log != nullptr);
+    if (dv == 32) {  // (64 ranks only)
+        if (pv != 64) return ROUTEPACK_E_UNSUPPORTED;
+        return a.lv == 2 ? chain_launch_v<64, 32, 2>(v, a, stream) : chain_launch_v<64, 32, 1>(v, a, stream);
+    }
     return dv == 8 ? chain_launch_d<8>(v, a, pv, stream) : chain_launch_d<16>(v, a, pv, stream);
 }
 

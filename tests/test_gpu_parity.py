@@ -304,6 +304,69 @@ def test_anneal_many_layers(case, kernel, monkeypatch):
     _compare_anneal(g, o)
 
 
+# 64 expert-parallel ranks (the largest window's rank count): the per-level
+# chain kernel forms a 64-rank row 16 ranks at a time, puts a row-shard's
+# cells on all 32 lanes of a half (up to 32 slots), and keeps the cell array
+# and the lengths in HBM.
+RANKS64 = {
+    "p64_l40_d8": dict(n=200, layers=40, experts=128, top_k=8, ranks=64, dp=8, edp=1),
+    "p64_l24_d32": dict(n=300, layers=24, experts=64, top_k=8, ranks=64, dp=32, edp=1),
+    "p64_l64_g2": dict(n=200, layers=64, experts=128, top_k=8, ranks=64, dp=8, edp=2),
+}
+
+
+def _ranks64_case(case, seed_base=80):
+    import oracle as O
+    shape = dict(cap=4096, tmin=64, tmax=1500, pop=32, levels=12)
+    shape.update(RANKS64[case])
+    w = synth.make_tiny_random(seed_base + sorted(RANKS64).index(case), **shape)
+    pd = synth.window_problem(w)
+    pb = O.Problem.from_dict(pd)
+    slot, _ = O.place(O.aggregate(w.demand), w.n_ranks)
+    q = O.project(w.demand, slot, w.n_ranks)
+    pr = O.pack_rows(pb, w.lengths, q, w.seed_pack, 8, 3, w.pop)
+    assert pr["rc"] == 0
+    return w, pd, pb, q, pr
+
+
+@gpu
+@pytest.mark.parametrize("case,kernel", [(c, k) for c in sorted(RANKS64) for k in ("chain", "wave", "workgroup")])
+def test_anneal_64_ranks(case, kernel, monkeypatch):
+    """Full trajectories (12 levels of 256 proposals, population 32) with 64
+    ranks on the per-level chain kernel and the two flat kernels."""
+    import oracle as O
+    rp = _rp()
+    _use_kernel(monkeypatch, kernel)
+    w, pd, pb, q, pr = _ranks64_case(case)
+    temps = synth.anneal_temperatures(w.levels)
+    _log(f"anneal {case}: R={pr['r_star']}, {w.levels} levels, {kernel} kernel")
+    o = O.anneal(pb, w.lengths, q, pr["r_star"], pr["population"], temps, 256, w.seed_anneal)
+    assert o["rc"] == 0
+    g = rp.anneal(rp.Problem.from_dict(pd), w.lengths, q, pr["r_star"], pr["population"], temps, 256,
+                  w.seed_anneal)
+    assert g["level_kernel"] == kernel
+    _compare_anneal(g, o)
+
+
+@gpu
+def test_anneal_64_ranks_not_in_one_launch(monkeypatch):
+    """The whole-schedule kernel is not compiled for 64 ranks: asking for it
+    fails with E_UNSUPPORTED, and without a request the per-level chain
+    kernel runs."""
+    rp = _rp()
+    w, pd, pb, q, pr = _ranks64_case("p64_l40_d8")
+    temps = synth.anneal_temperatures(w.levels)[:2]
+    _use_kernel(monkeypatch, "chain_run")
+    with pytest.raises(rp.RoutepackError) as ei:
+        rp.anneal(rp.Problem.from_dict(pd), w.lengths, q, pr["r_star"], pr["population"], temps, 256,
+                  w.seed_anneal)
+    assert ei.value.code == -8
+    monkeypatch.delenv("ROUTEPACK_ANNEAL_KERNEL")
+    g = rp.anneal(rp.Problem.from_dict(pd), w.lengths, q, pr["r_star"], pr["population"], temps, 256,
+                  w.seed_anneal)
+    assert g["level_kernel"] == "chain"
+
+
 # Degenerate shapes: no MoE layer (the rows are empty), a population that
 # fills no workgroup, a level size that is not a multiple of the batch of 64,
 # one DP slot, one proposal per level, and one row of two one-sample cells
