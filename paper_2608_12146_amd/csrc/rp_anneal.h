@@ -52,6 +52,9 @@ struct AnnealArgs {
     int32_t rv;                 // chain kernel: row-shards per lane (1 up to 64 row-shards, 2 up to 128)
     int32_t lv;                 // chain kernel: layers per lane (1 up to 32 layers, 2 up to 64)
     int32_t cg;                 // chain kernel: the cell array and the lengths stay in HBM, not LDS
+    int32_t hq;                 // chain kernel (64 ranks): Q in the slab and the cost prefixes in gcp, not LDS
+    int64_t *gcp;               // [pop][cp_stride] cost prefixes and totals of each member (hq)
+    int32_t cp_stride;
     int32_t dv, o_hcnt, o_hcell;  // chain kernel: cost-prefix stride; row-shard slot tables (shared)
     int32_t scale_pow2;         // 2^F C is a power of two
     double inv_scale;           // 1 / (2^F C) when it is

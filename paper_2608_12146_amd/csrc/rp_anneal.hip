@@ -1138,6 +1138,10 @@ extern "C" int routepack_anneal(const routepack_problem *prob, const int32_t *le
         int32_t *qt = scr.get<int32_t>(LP64 > 0 ? (size_t)N * LP64 : 1);
         if (scr.failed()) return ROUTEPACK_E_DEVICE;
         RP_TRY(chain_prepare(a, qt, stream));
+        if (a.hq) {  // (64 ranks: the members' cost prefixes live in HBM)
+            a.gcp = scr.get<int64_t>((size_t)pop_size * (size_t)a.cp_stride);
+            if (scr.failed()) return ROUTEPACK_E_DEVICE;
+        }
     }
     const bool fast = whole || chain || (want_wave && wave_plan(a, n_cu, &mpw, &tlds));
     if (!fast && !want_group) return ROUTEPACK_E_UNSUPPORTED;

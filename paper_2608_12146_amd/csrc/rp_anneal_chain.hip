@@ -532,10 +532,13 @@ __device__ inline Tables load_tables(const AnnealArgs &a, char *smem) {
     const int32_t RG = a.RG, DVr = a.dv;
     int32_t *s_hcnt = reinterpret_cast<int32_t *>(smem + a.o_hcnt);
     int32_t *s_hcell = reinterpret_cast<int32_t *>(smem + a.o_hcell);
+    // (hq layout with one EDP shard: no slot table, a row-shard's cells are
+    // h D + x)
+    const bool hcell = !(a.hq && G == 1);
     for (int32_t x = threadIdx.x; x < RG * DVr; x += blockDim.x) {
         const int32_t h = x / DVr, k = x - h * DVr, r = h / G, g = h - r * G, cnt = a.count[g];
         if (k == 0) s_hcnt[h] = cnt;
-        s_hcell[x] = r * D + a.slots[g * D + (k < cnt ? k : cnt - 1)];
+        if (hcell) s_hcell[x] = r * D + a.slots[g * D + (k < cnt ? k : cnt - 1)];
     }
     if (a.cg) {  // the lengths are read from HBM (L2)
         __syncthreads();
@@ -569,7 +572,7 @@ __device__ inline Lds member_lds(const AnnealArgs &a, char *smem, int wv) {
 // A member's state from a slab into LDS and registers (one wave).  The
 // global loads go out in batches of 16 per lane per array before any LDS
 // store, so a reload costs few memory round trips.
-template <int RV>
+template <int RV, bool HQ = false>
 __device__ inline void member_load(const AnnealArgs &a, const Lds &M, const Tables &tb, const SlabPtrs &g,
                                    Regs &R) {
     const int lane = lane_id();
@@ -614,7 +617,7 @@ __device__ inline void member_load(const AnnealArgs &a, const Lds &M, const Tabl
             if (x <= B) sv[u] = g.start[x];
             if (x < B) {
                 tv[u] = g.T[x];
-                qv[u] = g.Q[x];
+                if (!HQ) qv[u] = g.Q[x];  // (HQ: Q is used in place in the slab)
             }
         }
 #pragma unroll
@@ -623,7 +626,7 @@ __device__ inline void member_load(const AnnealArgs &a, const Lds &M, const Tabl
             if (x <= B) M.start[x] = (uint16_t)sv[u];
             if (x < B) {
                 M.T[x] = (int32_t)tv[u];
-                M.Q[x] = qv[u];
+                if (!HQ) M.Q[x] = qv[u];
             }
         }
     }
@@ -640,7 +643,7 @@ __device__ inline void member_load(const AnnealArgs &a, const Lds &M, const Tabl
         int64_t *cp = M.Cp + h * (a.dv + 1);
         for (int32_t x = 0; x < a.dv; ++x) {
             if (x < cnt) {
-                const int32_t c = tb.hcell[h * a.dv + x];
+                const int32_t c = HQ && G == 1 ? h * a.D + x : tb.hcell[h * a.dv + x];
                 const int64_t t = M.T[c], q = M.Q[c];
                 for (int s = 0; s < a.S; ++s) acc += a.alpha[s] * t + a.beta[s] * q;
                 cp[x] = acc;
@@ -666,8 +669,9 @@ __device__ inline void member_load(const AnnealArgs &a, const Lds &M, const Tabl
     wsync();
 }
 
-// A member's state back to a slab (W is kept up to date in the slab).
-template <int RV>
+// A member's state back to a slab (W is kept up to date in the slab, and Q
+// too with HQ).
+template <int RV, bool HQ = false>
 __device__ inline void member_store(const AnnealArgs &a, const Lds &M, const SlabPtrs &g, const Regs &R) {
     const int lane = lane_id();
     const int32_t N = a.N, B = a.B, RG = a.RG;
@@ -690,7 +694,7 @@ __device__ inline void member_store(const AnnealArgs &a, const Lds &M, const Sla
     for (int32_t x = lane; x <= B; x += kWave) g.start[x] = M.start[x];
     for (int32_t x = lane; x < B; x += kWave) {
         g.T[x] = M.T[x];
-        g.Q[x] = M.Q[x];
+        if (!HQ) g.Q[x] = M.Q[x];
     }
     if (lane < RG) {
         g.J[lane] = R.Jr;
@@ -1205,12 +1209,18 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain(AnnealArg
     Lds M = member_lds(a, smem, wv);
     const SlabPtrs g = slab_ptrs(a, a.slabs + (int64_t)a.slab_of[m] * a.off.bytes);
     M.gcell = g.cell;
+    constexpr bool HQ = PV == 64;  // (64 ranks: the hq layout)
+    if constexpr (HQ) {
+        M.Q = g.Q;
+        M.Cp = a.gcp + (int64_t)m * a.cp_stride;
+        M.Ctot = M.Cp + a.RG * (a.dv + 1);
+    }
     Regs R;
-    member_load<GV == 2 ? 2 : 1>(a, M, tb, g, R);
+    member_load<GV == 2 ? 2 : 1, HQ>(a, M, tb, g, R);
     member_level<PV, DV, GV, LV, CG>(a, M, tb, g.W, m, a.level, a.temp, a.xscore[0], a.xscore[1], a.xscore[2],
                          a.step_log ? a.step_log + (int64_t)m * a.K : nullptr, a.results + (int64_t)m * kRes,
                          nullptr, R);
-    member_store<GV == 2 ? 2 : 1>(a, M, g, R);
+    member_store<GV == 2 ? 2 : 1, HQ>(a, M, g, R);
 }
 
 // ---------------------------------------------------------------------------
@@ -1839,6 +1849,12 @@ bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out,
         if ((1 << sh) == a.D) a.dshift = sh;
     auto up16 = [](int64_t x) { return (x + 15) & ~(int64_t)15; };
     auto up8e = [](int64_t n) { return ((n + 7) & ~(int64_t)7) + 16; };  // elements, padded for 16-byte steps
+    // 64 ranks: Q stays in the slab and the cost prefixes in a per-member
+    // HBM array (a member's LDS is then its pool, start offsets, cell loads
+    // and roulette prefixes, about 77 KB for the largest window)
+    const bool hq = P == 64;
+    a.hq = hq ? 1 : 0;
+    a.cp_stride = hq ? (int32_t)((((int64_t)a.RG * (dv + 1) + a.RG) + 3) & ~(int64_t)3) : 0;
     // LDS of one member and of the workgroup's shared tables; with cg the
     // cell array stays in the slab and the lengths are read from HBM.
     auto layout = [&](bool cg, int64_t *shared_out) -> int64_t {
@@ -1847,13 +1863,13 @@ bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out,
         a.o_pool = (int32_t)o; o = up16(o + 2 * up8e(a.N));
         a.o_start = (int32_t)o; o = up16(o + 2 * up8e((int64_t)a.B + 1));
         a.o_T = (int32_t)o; o = up16(o + 4 * (int64_t)a.B);
-        a.o_Q = (int32_t)o; o = up16(o + 8 * (int64_t)a.B);
-        a.o_acost = (int32_t)o; o = up16(o + 8 * ((int64_t)a.RG * (dv + 1) + a.RG));  // cost prefixes and totals
+        a.o_Q = (int32_t)o; o = up16(o + (hq ? 0 : 8 * (int64_t)a.B));
+        a.o_acost = (int32_t)o; o = up16(o + (hq ? 0 : 8 * ((int64_t)a.RG * (dv + 1) + a.RG)));  // cost prefixes and totals
         a.o_Jpre = (int32_t)o; o = up16(o + 8 * 144 * (int64_t)a.rv);  // J_pre, V_pre and their pivots
         a.o_Jpiv = a.o_Jpre + 8 * 128 * a.rv;
         int64_t tab = up16(4 * ((int64_t)a.G * a.D + 2 * a.G + a.D));
         a.o_hcnt = (int32_t)tab; tab = up16(tab + 4 * (int64_t)a.RG);
-        a.o_hcell = (int32_t)tab; tab = up16(tab + 4 * (int64_t)a.RG * dv);
+        a.o_hcell = (int32_t)tab; tab = up16(tab + (hq && a.G == 1 ? 0 : 4 * (int64_t)a.RG * dv));
         a.o_tshared = (int32_t)tab;
         *shared_out = up16(tab + (cg ? 0 : 4 * (int64_t)a.N));
         return o;
