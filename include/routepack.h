@@ -192,9 +192,9 @@ typedef struct routepack_anneal_params {
  *              each member's cell array and the lengths in HBM to fit more
  *              members per CU (ROUTEPACK_CHAIN_LAYOUT=hbm asks for that
  *              layout, =lds forbids it); P = 64 always runs that layout, with
- *              the cells' squared-length sums and the cost prefixes in HBM
- *              too (a 64-rank row is formed 16 ranks at a time), per level
- *              only
+ *              the member pool, the cells' squared-length sums and the cost
+ *              prefixes in HBM too (a 64-rank row is formed 16 ranks at a
+ *              time), per level only
  *   WAVE       one wave per member, lanes over flat 64-entry strides:
  *              R G <= 512, member state within LDS
  *   WORKGROUP  one workgroup per member, state in HBM: every problem within

@@ -73,6 +73,7 @@ __device__ inline int64_t row_head_max64(int64_t v) {
 struct Lds {
     uint16_t *cell, *pool, *start;
     int32_t *gcell;  // the cell array in the member's slab instead (CG layout)
+    int32_t *gpool;  // the pool in the member's slab instead (64 ranks)
     int32_t *T;
     int64_t *Q;
     // [RG][DV + 1] prefix of the cell costs of each row-shard, slot order;
@@ -175,7 +176,7 @@ __device__ inline int32_t cell_of(const Lds &M, int32_t i) {
 // count D, one attention stage (S == 1), 32-bit layer sums, a power-of-two
 // score scale and no step log; GV == 0 takes all of these from the arguments.
 // RV is the number of row-shards per lane (2 for 65 to 128 row-shards).
-template <int DV, int GV, int RV, bool CG>
+template <int DV, int GV, int RV, bool CG, bool HP = false>
 __device__ inline Screen screen(const AnnealArgs &a, const Lds &M, const Tables &tb, uint64_t w0, uint64_t w1,
                                 uint64_t w2, uint64_t w3, uint64_t w4, uint64_t w5, uint64_t w6, int64_t s1,
                                 int64_t s2) {
@@ -285,7 +286,7 @@ __device__ inline Screen screen(const AnnealArgs &a, const Lds &M, const Tables 
     const int32_t pi = clamp0(st1 + (int32_t)bounded_small(w3, (uint32_t)(en1 - st1)), N - 1);
     const int32_t pj = clamp0(st2 + (int32_t)bounded_small(w6, (uint32_t)(en2 - st2)), N - 1);
     // stage 5: the samples; stage 6: their lengths
-    int32_t gi = M.pool[pi], gj = M.pool[pj];
+    int32_t gi = HP ? M.gpool[pi] : M.pool[pi], gj = HP ? M.gpool[pj] : M.pool[pj];
     stage_end(gi, gj);
     int32_t gti = tb.t[gi], gtj = tb.t[gj];
     stage_end(gti, gtj);
@@ -402,6 +403,64 @@ __device__ inline void pool_move(uint16_t *pool16, int32_t from, int32_t to, uin
         if (lane == 0) pool16[to] = (uint16_t)v;
         wsync();
     }
+}
+
+// count_less on an int32 pool in global memory (64 ranks).
+__device__ inline int32_t count_less_g(const int32_t *pool, int32_t lo, int32_t hi, int32_t v, int32_t skip) {
+    int32_t cnt = 0;
+    const int lane = lane_id();
+    for (int32_t b = lo; b < hi; b += kWave) {
+        const int32_t x = b + lane;
+        bool pred = false;
+        if (x < hi) {
+            const int32_t y = pool[x];
+            pred = (y < v) && (y != skip);
+        }
+        cnt += __popcll(__ballot(pred));
+    }
+    return cnt;
+}
+
+// pool_move on an int32 pool in global memory (64 ranks): each batch loads
+// all of its entries before it stores any, and the batches walk in the
+// direction of the shift, so no load reads an entry an earlier batch wrote.
+__device__ inline void pool_move_g(int32_t *pool, int32_t from, int32_t to, int32_t v) {
+    const int lane = lane_id();
+    constexpr int U = 8;
+    if (from < to) {
+        // new[x] = old[x + 1] for from <= x < to
+        for (int32_t base = from; base < to; base += U * kWave) {
+            int32_t val[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int32_t x = base + u * kWave + lane;
+                val[u] = x < to ? pool[x + 1] : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int32_t x = base + u * kWave + lane;
+                if (x < to) pool[x] = val[u];
+            }
+        }
+    } else if (from > to) {
+        // new[x] = old[x - 1] for to < x <= from (high batches first)
+        for (int32_t top = from; top > to; top -= U * kWave) {
+            int32_t val[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int32_t x = top - u * kWave - lane;
+                val[u] = x > to ? pool[x - 1] : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int32_t x = top - u * kWave - lane;
+                if (x > to) pool[x] = val[u];
+            }
+        }
+    }
+    wsync();
+    if (lane == 0) pool[to] = v;
+    wsync();
 }
 
 // start[c] += d for lo < c <= hi (16-bit entries, 32-bit words four per lane).
@@ -578,7 +637,7 @@ __device__ inline void member_load(const AnnealArgs &a, const Lds &M, const Tabl
     const int lane = lane_id();
     const int32_t N = a.N, B = a.B, RG = a.RG, G = a.G;
     constexpr int U = 16;
-    {
+    if (!(HQ && a.cg)) {  // (64 ranks: the cell array and the pool stay in the slab)
         const int32_t n4 = N >> 2;
         const int4 *c4 = reinterpret_cast<const int4 *>(g.cell), *p4 = reinterpret_cast<const int4 *>(g.pool);
         ushort4 *lc4 = reinterpret_cast<ushort4 *>(M.cell), *lp4 = reinterpret_cast<ushort4 *>(M.pool);
@@ -679,17 +738,19 @@ __device__ inline void member_store(const AnnealArgs &a, const Lds &M, const Sla
     const int32_t n4 = N >> 2;
     int4 *c4 = reinterpret_cast<int4 *>(g.cell), *p4 = reinterpret_cast<int4 *>(g.pool);
     const ushort4 *lc4 = reinterpret_cast<const ushort4 *>(M.cell), *lp4 = reinterpret_cast<const ushort4 *>(M.pool);
-    for (int32_t x = lane; x < n4; x += kWave) {
-        const ushort4 v = lp4[x];
-        if (!a.cg) {  // (CG layout: the slab's cell array is already current)
-            const ushort4 u = lc4[x];
-            c4[x] = make_int4(u.x, u.y, u.z, u.w);
+    if (!(HQ && a.cg)) {  // (64 ranks: the slab's cell array and pool are already current)
+        for (int32_t x = lane; x < n4; x += kWave) {
+            const ushort4 v = lp4[x];
+            if (!a.cg) {  // (CG layout: the slab's cell array is already current)
+                const ushort4 u = lc4[x];
+                c4[x] = make_int4(u.x, u.y, u.z, u.w);
+            }
+            p4[x] = make_int4(v.x, v.y, v.z, v.w);
         }
-        p4[x] = make_int4(v.x, v.y, v.z, v.w);
-    }
-    for (int32_t x = (n4 << 2) + lane; x < N; x += kWave) {
-        if (!a.cg) g.cell[x] = M.cell[x];
-        g.pool[x] = M.pool[x];
+        for (int32_t x = (n4 << 2) + lane; x < N; x += kWave) {
+            if (!a.cg) g.cell[x] = M.cell[x];
+            g.pool[x] = M.pool[x];
+        }
     }
     for (int32_t x = lane; x <= B; x += kWave) g.start[x] = M.start[x];
     for (int32_t x = lane; x < B; x += kWave) {
@@ -723,6 +784,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                                         int32_t level, double temp, int64_t x0, int64_t x1, int64_t x2,
                                         uint8_t *log_arg, int64_t *res, int64_t *trace_row, Regs &R) {
     constexpr int RV = GV == 2 ? 2 : 1;
+    constexpr bool HP = PV == 64;  // (64 ranks: the pool is in the slab)
     uint8_t *const log = GV == 1 ? nullptr : log_arg;  // (the common shape is launched without a step log)
     const int lane = lane_id();
     const int32_t N = a.N, B = a.B, RG = a.RG, D = a.D, G = GV == 1 ? 1 : a.G, L = a.L;
@@ -818,7 +880,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
         const uint64_t w0 = b0w.v[0], w1 = b0w.v[1], w2 = b0w.v[2], w3 = b0w.v[3];
         const uint64_t w4 = b1w.v[0], w5 = b1w.v[1], w6 = b1w.v[2], w7 = b1w.v[3];
         uint64_t pending = __ballot(k < a.K);
-        Screen sc = screen<DV, GV, RV, CG>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
+        Screen sc = screen<DV, GV, RV, CG, HP>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
         uint64_t feas = __ballot(sc.feas && k < a.K);
         uint64_t valid = ~0ull;  // lanes whose screen is current
         while (pending) {
@@ -828,7 +890,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                 // current; otherwise screen the batch again.
                 const uint64_t stale = pending & ~valid;
                 if (stale && (!cand || (stale & (~stale + 1)) <= (cand & (~cand + 1)))) {
-                    sc = screen<DV, GV, RV, CG>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
+                    sc = screen<DV, GV, RV, CG, HP>(a, M, tb, w0, w1, w2, w3, w4, w5, w6, s1, s2);
                     feas = __ballot(sc.feas && k < a.K);
                     valid = ~0ull;
                     cand = pending & feas;
@@ -896,7 +958,7 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
             if (small) {
                 const int32_t sz = half ? sz2 : sz1;
                 yv = hl < sz;
-                if (yv) y = M.pool[(half ? st2 : st1) + hl];
+                if (yv) y = HP ? M.gpool[(half ? st2 : st1) + hl] : M.pool[(half ? st2 : st1) + hl];
             }
             if (cact) {
                 if (cc == c1) {
@@ -1053,18 +1115,27 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                     const int32_t pin = __popcll(lt & (half ? 0xFFFFFFFF00000000ull : 0xFFFFFFFFull));
                     const int32_t st = half ? st2 : st1;
                     if (yv) {
-                        if (y == out) M.pool[st + pin] = (uint16_t)in;
-                        else M.pool[st + hl - (out < y ? 1 : 0) + (in < y ? 1 : 0)] = (uint16_t)y;
+                        const int32_t at = y == out ? st + pin : st + hl - (out < y ? 1 : 0) + (in < y ? 1 : 0);
+                        const int32_t val = y == out ? in : y;
+                        if constexpr (HP) M.gpool[at] = val;
+                        else M.pool[at] = (uint16_t)val;
                     }
                     wsync();
                 } else {
-                    if (pos_i < 0) pos_i = st1 + count_less(M.pool, st1, en1, i, -1);
-                    if (pos_j < 0) pos_j = st2 + count_less(M.pool, st2, en2, j, -1);
-                    const int32_t to1 = st1 + count_less(M.pool, st1, en1, j, i);
-                    const int32_t to2 = st2 + count_less(M.pool, st2, en2, i, j);
+                    auto cl = [&](int32_t lo, int32_t hi, int32_t v, int32_t skip) {
+                        return HP ? count_less_g(M.gpool, lo, hi, v, skip) : count_less(M.pool, lo, hi, v, skip);
+                    };
+                    auto mv = [&](int32_t from, int32_t to, int32_t v) {
+                        if constexpr (HP) pool_move_g(M.gpool, from, to, v);
+                        else pool_move(M.pool, from, to, (uint32_t)v);
+                    };
+                    if (pos_i < 0) pos_i = st1 + cl(st1, en1, i, -1);
+                    if (pos_j < 0) pos_j = st2 + cl(st2, en2, j, -1);
+                    const int32_t to1 = st1 + cl(st1, en1, j, i);
+                    const int32_t to2 = st2 + cl(st2, en2, i, j);
                     wsync();
-                    pool_move(M.pool, clamp0(pos_i, N - 1), clamp0(to1, N - 1), (uint32_t)j);
-                    pool_move(M.pool, clamp0(pos_j, N - 1), clamp0(to2, N - 1), (uint32_t)i);
+                    mv(clamp0(pos_i, N - 1), clamp0(to1, N - 1), j);
+                    mv(clamp0(pos_j, N - 1), clamp0(to2, N - 1), i);
                 }
             } else {
                 int32_t rk;
@@ -1074,12 +1145,14 @@ __device__ inline LevelOut member_level(const AnnealArgs &a, const Lds &M, const
                     if (pos_i < 0) pos_i = st1 + __popcll(b1);
                     rk = __popcll(b2);
                 } else {
-                    if (pos_i < 0) pos_i = st1 + count_less(M.pool, st1, en1, i, -1);
-                    rk = count_less(M.pool, st2, en2, i, -1);
+                    if (pos_i < 0)
+                        pos_i = st1 + (HP ? count_less_g(M.gpool, st1, en1, i, -1) : count_less(M.pool, st1, en1, i, -1));
+                    rk = HP ? count_less_g(M.gpool, st2, en2, i, -1) : count_less(M.pool, st2, en2, i, -1);
                 }
                 const int32_t to = c1 < c2 ? st2 - 1 + rk : st2 + rk;
                 wsync();
-                pool_move(M.pool, clamp0(pos_i, N - 1), clamp0(to, N - 1), (uint32_t)i);
+                if constexpr (HP) pool_move_g(M.gpool, clamp0(pos_i, N - 1), clamp0(to, N - 1), i);
+                else pool_move(M.pool, clamp0(pos_i, N - 1), clamp0(to, N - 1), (uint32_t)i);
                 if (c1 < c2) start_add(M.start, c1, c2, -1);
                 else start_add(M.start, c2, c1, 1);
             }
@@ -1211,6 +1284,7 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain(AnnealArg
     M.gcell = g.cell;
     constexpr bool HQ = PV == 64;  // (64 ranks: the hq layout)
     if constexpr (HQ) {
+        M.gpool = g.pool;
         M.Q = g.Q;
         M.Cp = a.gcp + (int64_t)m * a.cp_stride;
         M.Ctot = M.Cp + a.RG * (a.dv + 1);
@@ -1849,9 +1923,9 @@ bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out,
         if ((1 << sh) == a.D) a.dshift = sh;
     auto up16 = [](int64_t x) { return (x + 15) & ~(int64_t)15; };
     auto up8e = [](int64_t n) { return ((n + 7) & ~(int64_t)7) + 16; };  // elements, padded for 16-byte steps
-    // 64 ranks: Q stays in the slab and the cost prefixes in a per-member
-    // HBM array (a member's LDS is then its pool, start offsets, cell loads
-    // and roulette prefixes, about 77 KB for the largest window)
+    // 64 ranks: the pool and Q stay in the slab and the cost prefixes in a
+    // per-member HBM array (a member's LDS is then its start offsets, cell
+    // loads and roulette prefixes, about 13 KB for the largest window)
     const bool hq = P == 64;
     a.hq = hq ? 1 : 0;
     a.cp_stride = hq ? (int32_t)((((int64_t)a.RG * (dv + 1) + a.RG) + 3) & ~(int64_t)3) : 0;
@@ -1860,7 +1934,7 @@ bool chain_plan(AnnealArgs &a, int32_t n_cu, int32_t max_count, int32_t *pv_out,
     auto layout = [&](bool cg, int64_t *shared_out) -> int64_t {
         int64_t o = 0;
         a.o_cell = (int32_t)o; o = up16(o + (cg ? 0 : 2 * (int64_t)a.N));
-        a.o_pool = (int32_t)o; o = up16(o + 2 * up8e(a.N));
+        a.o_pool = (int32_t)o; o = up16(o + (hq && cg ? 0 : 2 * up8e(a.N)));
         a.o_start = (int32_t)o; o = up16(o + 2 * up8e((int64_t)a.B + 1));
         a.o_T = (int32_t)o; o = up16(o + 4 * (int64_t)a.B);
         a.o_Q = (int32_t)o; o = up16(o + (hq ? 0 : 8 * (int64_t)a.B));
