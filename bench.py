@@ -492,7 +492,7 @@ def main():
     extra = None
     if not args.no_extra_windows and args.window == "mid":
         extra = {}
-        for name, nl in (("heavy", 20), ("stress", 3)):
+        for name, nl in (("heavy", 20), ("stress", 20)):
             progress(f"extra window {name}: {nl} levels")
             extra[name] = window_short_run(name, nl)
             progress(f"  {extra[name]['kernel']}: {extra[name]['move_evals_per_s_kernel']:.3e} move-evals/s "
