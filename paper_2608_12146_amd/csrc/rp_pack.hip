@@ -745,6 +745,10 @@ __global__ void __launch_bounds__(128) k_pack_cellsum(TrialArgs a, PackFast pf) 
 }
 
 // EDPAwarePair of candidate b (block per candidate).
+// WG: the trial's row-shard loads W stay in its slice of a.Wt in HBM (when
+// they do not fit LDS next to the rest); every W access is a coalesced
+// 16-byte read or an update of one row by the whole workgroup.
+template <bool WG>
 __global__ void __launch_bounds__(1024) k_pack_pair(TrialArgs a, PackFast pf) {
     extern __shared__ __align__(16) char spair[];
     __shared__ int32_t s_h;
@@ -756,8 +760,9 @@ __global__ void __launch_bounds__(1024) k_pack_pair(TrialArgs a, PackFast pf) {
     int64_t *after = reinterpret_cast<int64_t *>(spair);            // [RG]
     int64_t *pkv = after + RG, *base = pkv + RG;                    // [RG], [RG]
     int64_t *speak = base + RG;                                     // [K]
-    int32_t *Wl = reinterpret_cast<int32_t *>(speak + K + ((3 * RG + K) & 1));  // [RG][LP], 16-byte aligned
-    int32_t *qb = Wl + (int64_t)RG * LP;                            // [2][LP]
+    int32_t *lds_next = reinterpret_cast<int32_t *>(speak + K + ((3 * RG + K) & 1));  // 16-byte aligned
+    int32_t *Wl = WG ? a.Wt + (int64_t)b * RG * LP : lds_next;      // [RG][LP]
+    int32_t *qb = WG ? lds_next : Wl + (int64_t)RG * LP;            // [2][LP]
     int32_t *mxs = qb + 2 * LP;                                     // [RG][L]
     int32_t *filled = mxs + RG * L;                                 // [RG]
     int32_t *hcnt = filled + RG;                                    // [RG]
@@ -1132,8 +1137,13 @@ extern "C" int routepack_pack_rows(const routepack_problem *prob, const int32_t 
     // Seed trials: three kernels for the common shapes, else one.
     // ROUTEPACK_PACK_KERNEL=single requests the single-kernel path.
     const char *pk_force = getenv("ROUTEPACK_PACK_KERNEL");
-    const int64_t pair_lds = 8 * (3 * (int64_t)RG + K + 1) +
-                             4 * ((int64_t)RG * LP + 2 * LP + (int64_t)RG * prob->n_layers + 2 * (int64_t)RG + 2 * (int64_t)K);
+    // The pairing kernel keeps W in LDS when it fits (ROUTEPACK_PACK_W=hbm
+    // keeps it in HBM regardless), else in HBM.
+    const int64_t pair_rest = 8 * (3 * (int64_t)RG + K + 1) +
+                              4 * (2 * LP + (int64_t)RG * prob->n_layers + 2 * (int64_t)RG + 2 * (int64_t)K);
+    const char *pw_force = getenv("ROUTEPACK_PACK_W");
+    const bool w_hbm = (pw_force && strcmp(pw_force, "hbm") == 0) || pair_rest + 4 * (int64_t)RG * LP > 150 * 1024;
+    const int64_t pair_lds = pair_rest + (w_hbm ? 0 : 4 * (int64_t)RG * LP);
     const bool fast = !(pk_force && strcmp(pk_force, "single") == 0) && C < ((int64_t)1 << 31) && N < 65536 &&
                       prob->n_ranks >= 4 && LP > 0 && pair_lds <= 150 * 1024;
     if (fast) {
@@ -1143,15 +1153,16 @@ extern "C" int routepack_pack_rows(const routepack_problem *prob, const int32_t 
         if (scr.failed()) return ROUTEPACK_E_DEVICE;
         const size_t fit_lds = (size_t)16 * K;
         RP_HIP(hipFuncSetAttribute((const void *)k_pack_fit, hipFuncAttributeMaxDynamicSharedMemorySize, (int)fit_lds));
-        RP_HIP(hipFuncSetAttribute((const void *)k_pack_pair, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                   (int)pair_lds));
+        const void *pair_fn = w_hbm ? (const void *)k_pack_pair<true> : (const void *)k_pack_pair<false>;
+        RP_HIP(hipFuncSetAttribute(pair_fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)pair_lds));
         if (K <= 8 * kWave) {
             hipLaunchKernelGGL(k_pack_fit_reg<8>, dim3(nb), dim3(64), (size_t)8 * K, stream, ta, pf);
         } else {
             hipLaunchKernelGGL(k_pack_fit, dim3(nb), dim3(64), fit_lds, stream, ta, pf);
         }
         hipLaunchKernelGGL(k_pack_cellsum, dim3(K, nb), dim3(128), (size_t)4 * LP, stream, ta, pf);
-        hipLaunchKernelGGL(k_pack_pair, dim3(nb), dim3(1024), (size_t)pair_lds, stream, ta, pf);
+        if (w_hbm) hipLaunchKernelGGL(k_pack_pair<true>, dim3(nb), dim3(1024), (size_t)pair_lds, stream, ta, pf);
+        else hipLaunchKernelGGL(k_pack_pair<false>, dim3(nb), dim3(1024), (size_t)pair_lds, stream, ta, pf);
     } else {
         hipLaunchKernelGGL(k_pack_trials, dim3(nb), dim3(64), 0, stream, ta);
     }

@@ -496,16 +496,20 @@ def test_anneal_crowded_cells(G, kernel, monkeypatch):
 @gpu
 @pytest.mark.parametrize("name,G,S", [("tiny", 1, 1), ("tiny", 2, 1), ("small", 1, 1), ("small", 4, 1),
                                       ("mid", 1, 1), ("mid", 2, 1), ("small", 2, 2), ("mid", 1, 2)])
-@pytest.mark.parametrize("path", ["default", "single"])
+@pytest.mark.parametrize("path", ["default", "single", "w_hbm"])
 def test_pack_rows(name, G, S, path, monkeypatch):
     """Row count and seed population equal to the oracle's; "single" requests
     the one-kernel seed trials, "default" the library's choice (three
-    kernels where the shape allows)."""
+    kernels where the shape allows), "w_hbm" the three kernels with the
+    pairing's row-shard loads in HBM (the largest windows' path)."""
     rp = _rp()
+    monkeypatch.delenv("ROUTEPACK_PACK_W", raising=False)
     if path == "single":
         monkeypatch.setenv("ROUTEPACK_PACK_KERNEL", "single")
     else:
         monkeypatch.delenv("ROUTEPACK_PACK_KERNEL", raising=False)
+    if path == "w_hbm":
+        monkeypatch.setenv("ROUTEPACK_PACK_W", "hbm")
     _log(f"pack_rows {name} G={G} S={S} ({path} seed trials)")
     w, pd, pb, agg, slot, load, q = _window(name, G, S)
     pr = _packed(name, G, S)
