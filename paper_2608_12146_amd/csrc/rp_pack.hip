@@ -667,18 +667,16 @@ __global__ void __launch_bounds__(64) k_pack_fit_reg(TrialArgs a, PackFast pf) {
                 }
                 c = 0xFFFF - (int32_t)(best & 0xFFFF);
             }
-            // c is uniform: only its chunk's owner lane changes
+            // c is uniform: only its chunk's owner lane changes (a uniform
+            // branch per chunk, so every register index stays static)
             const int32_t cu = c >> 6;
             const bool own = (c & (kWave - 1)) == lane;
 #pragma unroll
             for (int u = 0; u < NCH; ++u)
-                if (u == cu) {
-                    if (own) {
-                        Tr[u] += ti;
-                        nr[u] += 1;
-                        kr[u] = fit_key(Tr[u], nr[u], c);
-                    }
-                    break;
+                if (u == cu && own) {
+                    Tr[u] += ti;
+                    nr[u] += 1;
+                    kr[u] = fit_key(Tr[u], nr[u], c);
                 }
             if (lane == 0) cellk[item] = c;
         }
@@ -1157,6 +1155,8 @@ extern "C" int routepack_pack_rows(const routepack_problem *prob, const int32_t 
         RP_HIP(hipFuncSetAttribute(pair_fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)pair_lds));
         if (K <= 8 * kWave) {
             hipLaunchKernelGGL(k_pack_fit_reg<8>, dim3(nb), dim3(64), (size_t)8 * K, stream, ta, pf);
+        } else if (K <= 32 * kWave) {
+            hipLaunchKernelGGL(k_pack_fit_reg<32>, dim3(nb), dim3(64), (size_t)8 * K, stream, ta, pf);
         } else {
             hipLaunchKernelGGL(k_pack_fit, dim3(nb), dim3(64), fit_lds, stream, ta, pf);
         }
