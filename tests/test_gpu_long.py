@@ -79,8 +79,9 @@ def test_anneal_full_schedule_large(name):
     2048; about eleven minutes of oracle time, reported every 50 levels) and
     the first 4 of the stress window's 500 (population 4096; about two and a
     half minutes of oracle time per level, reported every level), on
-    whichever level kernel the library picks (more than 32 layers rule out
-    the chain kernels)."""
+    whichever level kernel the library picks (the per-level chain kernel:
+    the cell array and lengths in HBM for the heavy-tail window, the 64-rank
+    layout for the stress window)."""
     if name == "heavy":
         _full_schedule(name, 1, chunk=50, kernel=None, levels=1000)
     else:
