@@ -552,9 +552,14 @@ __global__ void __launch_bounds__(64) k_pack_fit(TrialArgs a, PackFast pf) {
     }
 }
 
-// k_pack_fit for K <= 64 NCH cells: lane x holds the load, member count and
-// key of cells x, x + 64, ... in registers, so the ranked passes need no LDS
-// traffic and a placement updates one lane.
+// k_pack_fit for K <= 64 NCH cells: lane x holds the keys of cells x,
+// x + 64, ... in registers, so the ranked passes need no LDS traffic and a
+// placement updates one lane.  A key carries the load in its high 32 bits
+// (C < 2^31) and 0xFFFF - members below, so "the item fits" is one compare,
+// key < (C - t + 1) << 32, and a placement adds (t << 32) - (1 << 16).  The
+// draws, the window's next items and their lengths are loaded one block of
+// 64 steps ahead, and each step's (item, cell) stays in the register of lane
+// (step mod 64) until its block ends, so no step waits on memory.
 template <int NCH>
 __global__ void __launch_bounds__(64) k_pack_fit_reg(TrialArgs a, PackFast pf) {
     extern __shared__ int32_t sfitr[];  // [K] counts, then [K] cursors
@@ -563,15 +568,11 @@ __global__ void __launch_bounds__(64) k_pack_fit_reg(TrialArgs a, PackFast pf) {
     const int32_t N = a.N, K = a.K;
     int32_t *cnt_s = sfitr, *cur = sfitr + K;
     int32_t *cellk = a.cellk + (int64_t)b * N;
-    int64_t Tr[NCH];
-    int32_t nr[NCH];
     uint64_t kr[NCH];
 #pragma unroll
     for (int u = 0; u < NCH; ++u) {
         const int32_t c = u * kWave + lane;
-        Tr[u] = 0;
-        nr[u] = 0;
-        kr[u] = c < K ? fit_key(0, 0, c) : 0;
+        kr[u] = c < K ? fit_key(0, 0, c) : ~(uint64_t)0;  // a missing cell never fits
     }
     int32_t good = 1;
     if (b == 0) {
@@ -591,20 +592,34 @@ __global__ void __launch_bounds__(64) k_pack_fit_reg(TrialArgs a, PackFast pf) {
             wint = a.t[win];
         }
         int32_t next = w < N ? w : N, wsize = next;
+        // items entering the window: this block (s0, t0), the next (s1, t1)
+        // and the items of the one after (s2), whose lengths are loaded when
+        // it becomes the next
         int32_t sbase = next;
-        int32_t sreg = sbase + lane < N ? a.sigma[sbase + lane] : 0;
-        int32_t streg = sbase + lane < N ? a.t[sreg] : 0;
+        const int32_t i0 = sbase + lane, i1 = i0 + kWave, i2 = i1 + kWave;
+        int32_t s0 = i0 < N ? a.sigma[i0] : 0, s1 = i1 < N ? a.sigma[i1] : 0;
+        int32_t s2 = i2 < N ? a.sigma[i2] : 0;
+        int32_t t0 = i0 < N ? a.t[s0] : 0, t1 = i1 < N ? a.t[s1] : 0;
+        // draws: shuffle word h and best-fit word h, this block and the next
         int32_t hbase = 0;
         uint64_t wr1 = lane < N ? wd[lane] : 0, wr2 = lane < N ? wd[N + lane] : 0;
+        uint64_t nw1 = kWave + lane < N ? wd[kWave + lane] : 0;
+        uint64_t nw2 = kWave + lane < N ? wd[N + kWave + lane] : 0;
+        int32_t p_item = -1, p_cell = 0;  // step hbase + lane's placement
         for (int32_t h = 0; h < N; ++h) {
             if (h - hbase == kWave) {
+                if (p_item >= 0) cellk[p_item] = p_cell;
+                p_item = -1;
                 hbase += kWave;
-                wr1 = hbase + lane < N ? wd[hbase + lane] : 0;
-                wr2 = hbase + lane < N ? wd[N + hbase + lane] : 0;
+                wr1 = nw1;
+                wr2 = nw2;
+                const int32_t hn = hbase + kWave + lane;
+                nw1 = hn < N ? wd[hn] : 0;
+                nw2 = hn < N ? wd[N + hn] : 0;
             }
             const int32_t pos = (int32_t)bounded(readlane64(wr1, h - hbase), (uint64_t)wsize);
             const int32_t item = __builtin_amdgcn_readlane(win, pos);
-            const int64_t ti = __builtin_amdgcn_readlane(wint, pos);
+            const int32_t ti = __builtin_amdgcn_readlane(wint, pos);
             int32_t up, upt;
             if (w <= 16) {  // row_shl:1 -- lane i reads lane i + 1 of its 16-lane row
                 up = __builtin_amdgcn_update_dpp(win, win, 0x101, 0xF, 0xF, false);
@@ -620,11 +635,15 @@ __global__ void __launch_bounds__(64) k_pack_fit_reg(TrialArgs a, PackFast pf) {
             if (next < N) {
                 if (next - sbase == kWave) {
                     sbase += kWave;
-                    sreg = sbase + lane < N ? a.sigma[sbase + lane] : 0;
-                    streg = sbase + lane < N ? a.t[sreg] : 0;
+                    s0 = s1;
+                    t0 = t1;
+                    s1 = s2;
+                    const int32_t j1 = sbase + kWave + lane, j2 = j1 + kWave;
+                    t1 = j1 < N ? a.t[s1] : 0;
+                    s2 = j2 < N ? a.sigma[j2] : 0;
                 }
-                const int32_t ni = __builtin_amdgcn_readlane(sreg, next - sbase);
-                const int32_t nt = __builtin_amdgcn_readlane(streg, next - sbase);
+                const int32_t ni = __builtin_amdgcn_readlane(s0, next - sbase);
+                const int32_t nt = __builtin_amdgcn_readlane(t0, next - sbase);
                 if (lane == wsize - 1) {
                     win = ni;
                     wint = nt;
@@ -641,14 +660,14 @@ __global__ void __launch_bounds__(64) k_pack_fit_reg(TrialArgs a, PackFast pf) {
             if (h < K) {
                 c = h;
             } else {
+                const uint64_t lim = ti <= a.C ? (uint64_t)(a.C - ti + 1) << 32 : 0;
                 uint64_t best = 0;
                 int32_t nf = 0;
-                bool fe[NCH];
 #pragma unroll
                 for (int u = 0; u < NCH; ++u) {
-                    fe[u] = u * kWave + lane < K && Tr[u] + ti <= a.C;
-                    nf += __popcll(__ballot(fe[u]));
-                    if (fe[u] && kr[u] > best) best = kr[u];
+                    const bool f = kr[u] < lim;
+                    nf += __popcll(__ballot(f));
+                    if (f && kr[u] > best) best = kr[u];
                 }
                 if (nf == 0) {
                     good = 0;
@@ -657,12 +676,13 @@ __global__ void __launch_bounds__(64) k_pack_fit_reg(TrialArgs a, PackFast pf) {
                 best = wave_max_u64(best);
                 const int32_t wp = w < nf ? w : nf;
                 const int32_t rho = (int32_t)bounded(readlane64(wr2, h - hbase), (uint64_t)wp);
+                // a key below a fitting key fits too
                 for (int32_t pass = 1; pass <= rho; ++pass) {
                     const uint64_t prev = best;
                     best = 0;
 #pragma unroll
                     for (int u = 0; u < NCH; ++u)
-                        if (fe[u] && kr[u] < prev && kr[u] > best) best = kr[u];
+                        if (kr[u] < prev && kr[u] > best) best = kr[u];
                     best = wave_max_u64(best);
                 }
                 c = 0xFFFF - (int32_t)(best & 0xFFFF);
@@ -671,18 +691,19 @@ __global__ void __launch_bounds__(64) k_pack_fit_reg(TrialArgs a, PackFast pf) {
             // branch per chunk, so every register index stays static)
             const int32_t cu = c >> 6;
             const bool own = (c & (kWave - 1)) == lane;
+            const uint64_t add = ((uint64_t)(uint32_t)ti << 32) - ((uint64_t)1 << 16);
 #pragma unroll
             for (int u = 0; u < NCH; ++u)
-                if (u == cu && own) {
-                    Tr[u] += ti;
-                    nr[u] += 1;
-                    kr[u] = fit_key(Tr[u], nr[u], c);
-                }
-            if (lane == 0) cellk[item] = c;
+                if (u == cu && own) kr[u] += add;
+            if (lane == h - hbase) {
+                p_item = item;
+                p_cell = c;
+            }
         }
+        if (p_item >= 0) cellk[p_item] = p_cell;
 #pragma unroll
         for (int u = 0; u < NCH; ++u)
-            if (u * kWave + lane < K) cnt_s[u * kWave + lane] = nr[u];
+            if (u * kWave + lane < K) cnt_s[u * kWave + lane] = 0xFFFF - (int32_t)((kr[u] >> 16) & 0xFFFF);
     }
     if (lane == 0) a.ok[b] = good;
     if (!good) return;
