@@ -16,12 +16,20 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  * - Arrays are C-order and live in DEVICE memory unless marked [host].  The
- *   caller owns every array; the library keeps no pointer after a call's
- *   stream work completes and frees its own scratch before returning
- *   (synchronous calls) or stream-ordered on `stream` (asynchronous calls).
+ *   caller owns every array; the library keeps no pointer to caller memory
+ *   after a call's stream work completes.
+ * - Scratch: each (device, stream) the library is called on keeps one
+ *   scratch arena from the device's stream-ordered memory pool, sized to the
+ *   largest scratch a call on that stream has needed and reused by the next
+ *   call there (the stream orders the two); arenas are held until the
+ *   process ends.  Scratch that does not fit the arena comes from the pool
+ *   and goes back to it before the call returns (synchronous calls) or
+ *   stream-ordered on `stream` (asynchronous calls).
  * - Work is enqueued on the caller's `stream`.  Calls marked "synchronizes"
- *   wait for that stream before returning.  There is no global mutable
- *   state; calls on different streams are independent.
+ *   wait for that stream before returning.  Results depend on the arguments
+ *   only; calls on different streams are independent (each stream has its
+ *   own arena; a second thread that calls on a stream while another thread's
+ *   call there is still in progress takes its scratch from the pool).
  * - Layout encoding: a layout is int32 [N] holding, for each sample i, its
  *   cell id c = r * D + d (row r in [0, R), DP slot d in [0, D)).  A
  *   row-shard is h = r * G + g with g = dp_to_edp[d].

@@ -1,8 +1,12 @@
 // Validation, scratch, window bounds and status strings for the RoutePack
 // C-ABI library.
 #include <atomic>
+#include <map>
 #include <math.h>
+#include <mutex>
 #include <string.h>
+#include <thread>
+#include <utility>
 
 #include "rp_device.h"
 #include "rp_internal.h"
@@ -53,15 +57,70 @@ static void keep_pool_memory() {
     (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &threshold);
 }
 
-Scratch::Scratch(hipStream_t s) : stream_(s) { keep_pool_memory(); }
+// One stream's scratch arena: [0, top) is held by the live Scratch objects
+// on it (nested calls stack), want is the largest extent a call has needed.
+struct Arena {
+    char *base = nullptr;
+    size_t cap = 0, top = 0, want = 0;
+    int depth = 0;
+    std::thread::id owner;
+};
+
+static std::mutex g_arena_mu;
+static std::map<std::pair<int, hipStream_t>, Arena> g_arenas;  // (device, stream); never erased
+
+Scratch::Scratch(hipStream_t s) : stream_(s) {
+    keep_pool_memory();
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return;
+    std::lock_guard<std::mutex> lock(g_arena_mu);
+    Arena &a = g_arenas[std::make_pair(dev, s)];
+    if (a.depth > 0 && a.owner != std::this_thread::get_id()) return;  // another thread's call: pool only
+    a.owner = std::this_thread::get_id();
+    depth_ = ++a.depth;
+    start_ = a.top;
+    arena_ = &a;
+}
 
 Scratch::~Scratch() {
     for (void *q : ptrs_) (void)hipFreeAsync(q, stream_);
+    if (!arena_) return;
+    std::lock_guard<std::mutex> lock(g_arena_mu);
+    Arena &a = *arena_;
+    constexpr size_t kGrain = (size_t)2 << 20;
+    const size_t peak = (start_ + need_ + kGrain - 1) & ~(kGrain - 1);
+    if (peak > a.want) a.want = peak;
+    a.top = start_;
+    --a.depth;
 }
 
 void *Scratch::alloc(size_t n) {
-    void *q = nullptr;
     n = (n + 255) & ~(size_t)255;
+    if (arena_) {
+        std::lock_guard<std::mutex> lock(g_arena_mu);
+        Arena &a = *arena_;
+        need_ += n;
+        if (depth_ == a.depth) {  // the innermost live Scratch: the top of the arena is its own
+            if (depth_ == 1 && a.top == 0 && a.want > a.cap) {
+                // grow before the outermost call's first piece; the old arena
+                // goes back to the pool in stream order
+                if (a.base) (void)hipFreeAsync(a.base, stream_);
+                a.base = nullptr;
+                a.cap = 0;
+                void *q = nullptr;
+                if (hipMallocAsync(&q, a.want, stream_) == hipSuccess) {
+                    a.base = static_cast<char *>(q);
+                    a.cap = a.want;
+                }
+            }
+            if (a.top + n <= a.cap) {
+                void *q = a.base + a.top;
+                a.top += n;
+                return q;
+            }
+        }
+    }
+    void *q = nullptr;
     if (hipMallocAsync(&q, n, stream_) != hipSuccess) {
         failed_ = true;
         return nullptr;

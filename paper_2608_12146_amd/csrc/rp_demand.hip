@@ -10,6 +10,7 @@
 // each column (the partials are at most 2/64 of the bytes read).  Integer
 // sums are exact, so the result does not depend on the order.
 #include <mutex>
+#include <optional>
 #include <type_traits>
 
 #include "rp_device.h"
@@ -394,11 +395,12 @@ static int aggregate_demand(const routepack_problem *prob, const int32_t *demand
     const int32_t band = (int32_t)((N + gy - 1) / gy);
     gy = (N + band - 1) / band;
     if (gx > 2147483647LL) return ROUTEPACK_E_UNSUPPORTED;
-    Scratch scr(stream);
+    std::optional<Scratch> scr;  // (none with a fixed partials buffer)
     int64_t *part = fixed;
     if (!part) {
-        part = scr.get<int64_t>((size_t)gy * M);
-        if (scr.failed()) return ROUTEPACK_E_DEVICE;
+        scr.emplace(stream);
+        part = scr->get<int64_t>((size_t)gy * M);
+        if (scr->failed()) return ROUTEPACK_E_DEVICE;
     }
     if (vec)
         hipLaunchKernelGGL(k_aggregate_bands<4>, dim3((unsigned)gx, (unsigned)gy), dim3(256), 0, stream, demand,

@@ -35,11 +35,22 @@ struct Topology {
 // Validates the sizes, coefficients and partition of a problem.
 int check_problem(const routepack_problem *p, Topology *topo);
 
-// RAII device scratch allocated stream-ordered on one stream.
+struct Arena;
+
+// RAII device scratch for one call on one stream.  Each (device, stream)
+// keeps an arena that the innermost live Scratch on it bump-allocates from;
+// the arena is sized to the largest total a call on that stream has asked
+// for and is reused by the next call (the stream orders the calls), so a
+// call costs no allocator round trips once the stream has seen its size.
+// What does not fit comes from the device's stream-ordered pool and goes
+// back to it when the Scratch ends.  Nothing is allocated before the first
+// alloc().  An arena lives until the process ends.
 class Scratch {
   public:
     explicit Scratch(hipStream_t s);
     ~Scratch();
+    Scratch(const Scratch &) = delete;
+    Scratch &operator=(const Scratch &) = delete;
     // Allocates n bytes (256-byte aligned); returns nullptr on failure.
     void *alloc(size_t n);
     template <class T>
@@ -48,7 +59,11 @@ class Scratch {
 
   private:
     hipStream_t stream_;
-    std::vector<void *> ptrs_;
+    Arena *arena_ = nullptr;  // this stream's arena (null: another thread holds it)
+    int depth_ = 0;           // nesting depth of this Scratch on the arena
+    size_t start_ = 0;        // arena offset when this Scratch began
+    size_t need_ = 0;         // bytes this Scratch asked for
+    std::vector<void *> ptrs_;  // pieces taken from the pool
     bool failed_ = false;
 };
 
