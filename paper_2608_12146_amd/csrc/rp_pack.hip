@@ -88,10 +88,32 @@ __global__ void __launch_bounds__(64) k_ffd(const int32_t *__restrict__ t, const
         const int64_t v = wave_max(c < K ? room[c] : -1);
         if (lane == x) cmax = v;
     }
+    // Items after the first K: this block's items and lengths (s0, t0), the
+    // next block's (s1, t1) and the items of the one after (s2), loaded a
+    // block of 64 ahead; item hb + x's cell stays in lane x until its block
+    // is stored, so no step waits on memory.  Only this wave touches the
+    // LDS rooms, so a wave-level fence orders a step's update before the
+    // next step's reads.
+    int32_t hb = K;
+    const int32_t i0 = hb + lane, i1 = i0 + kWave, i2 = i1 + kWave;
+    int32_t s0 = i0 < N ? sigma[i0] : 0, s1 = i1 < N ? sigma[i1] : 0, s2 = i2 < N ? sigma[i2] : 0;
+    int32_t t0 = i0 < N ? t[s0] : 0, t1 = i1 < N ? t[s1] : 0;
+    int32_t p_item = -1, p_cell = 0;
     int32_t good = 1;
     for (int32_t h = K; h < N; ++h) {
-        const int32_t i = sigma[h];
-        const int64_t ti = t[i];
+        if (h - hb == kWave) {
+            if (p_item >= 0) cell_of[p_item] = p_cell;
+            p_item = -1;
+            hb += kWave;
+            s0 = s1;
+            t0 = t1;
+            s1 = s2;
+            const int32_t j1 = hb + kWave + lane, j2 = j1 + kWave;
+            t1 = j1 < N ? t[s1] : 0;
+            s2 = j2 < N ? sigma[j2] : 0;
+        }
+        const int32_t i = __builtin_amdgcn_readlane(s0, h - hb);
+        const int64_t ti = __builtin_amdgcn_readlane(t0, h - hb);
         const uint64_t m1 = __ballot(lane < nchunk && cmax >= ti);
         if (!m1) {
             good = 0;
@@ -105,9 +127,15 @@ __global__ void __launch_bounds__(64) k_ffd(const int32_t *__restrict__ t, const
         if (c0 + lane == c) room[c] = nr;
         const int64_t nm = wave_max(nr);
         if (lane == x) cmax = nm;
-        if (lane == 0) cell_of[i] = c;
-        __syncthreads();
+        if (lane == h - hb) {
+            p_item = i;
+            p_cell = c;
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
+    if (p_item >= 0) cell_of[p_item] = p_cell;
     if (lane == 0) *ok = good;
 }
 
