@@ -889,10 +889,20 @@ __global__ void __launch_bounds__(1024) k_pack_pair(TrialArgs a, PackFast pf) {
         for (int32_t h = tid; h < RG; h += nt) {
             int64_t af = 0, pk = 0;
             if (filled[h] < hcnt[h]) {
-                for (int32_t l = 0; l < L; ++l) {
-                    const int32_t mx = mxs[h * L + l];
-                    af += mx;
-                    pk = mx > pk ? mx : pk;
+                if ((L & 3) == 0) {  // the row's maxima as 16-byte reads (mxs is 16-byte aligned)
+                    const int4 *m4 = reinterpret_cast<const int4 *>(mxs + h * L);
+                    for (int32_t l4 = 0; l4 < (L >> 2); ++l4) {
+                        const int4 v = m4[l4];
+                        af += (int64_t)v.x + v.y + v.z + v.w;
+                        const int32_t m = max(max(v.x, v.y), max(v.z, v.w));
+                        pk = m > pk ? m : pk;
+                    }
+                } else {
+                    for (int32_t l = 0; l < L; ++l) {
+                        const int32_t mx = mxs[h * L + l];
+                        af += mx;
+                        pk = mx > pk ? mx : pk;
+                    }
                 }
             }
             after[h] = af;
