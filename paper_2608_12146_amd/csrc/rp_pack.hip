@@ -633,6 +633,16 @@ __global__ void __launch_bounds__(64) k_pack_fit_reg(TrialArgs a, PackFast pf) {
         uint64_t wr1 = lane < N ? wd[lane] : 0, wr2 = lane < N ? wd[N + lane] : 0;
         uint64_t nw1 = kWave + lane < N ? wd[kWave + lane] : 0;
         uint64_t nw2 = kWave + lane < N ? wd[N + kWave + lane] : 0;
+        // Step hb + lane's window position (the window holds min(w, N - h)
+        // items at step h) and its rank when w or more cells fit, drawn when
+        // the block becomes current.
+        auto draws = [&](int32_t hb, int32_t &pos_l, int32_t &rho_l) {
+            const int32_t hh = hb + lane, ws = w < N - hh ? w : N - hh;
+            pos_l = hh < N ? (int32_t)bounded(wr1, (uint64_t)ws) : 0;
+            rho_l = (int32_t)bounded(wr2, (uint64_t)w);
+        };
+        int32_t pos_l, rho_l;
+        draws(0, pos_l, rho_l);
         int32_t p_item = -1, p_cell = 0;  // step hbase + lane's placement
         for (int32_t h = 0; h < N; ++h) {
             if (h - hbase == kWave) {
@@ -641,11 +651,12 @@ __global__ void __launch_bounds__(64) k_pack_fit_reg(TrialArgs a, PackFast pf) {
                 hbase += kWave;
                 wr1 = nw1;
                 wr2 = nw2;
+                draws(hbase, pos_l, rho_l);
                 const int32_t hn = hbase + kWave + lane;
                 nw1 = hn < N ? wd[hn] : 0;
                 nw2 = hn < N ? wd[N + hn] : 0;
             }
-            const int32_t pos = (int32_t)bounded(readlane64(wr1, h - hbase), (uint64_t)wsize);
+            const int32_t pos = __builtin_amdgcn_readlane(pos_l, h - hbase);
             const int32_t item = __builtin_amdgcn_readlane(win, pos);
             const int32_t ti = __builtin_amdgcn_readlane(wint, pos);
             int32_t up, upt;
@@ -702,8 +713,8 @@ __global__ void __launch_bounds__(64) k_pack_fit_reg(TrialArgs a, PackFast pf) {
                     break;
                 }
                 best = wave_max_u64(best);
-                const int32_t wp = w < nf ? w : nf;
-                const int32_t rho = (int32_t)bounded(readlane64(wr2, h - hbase), (uint64_t)wp);
+                const int32_t rho = nf >= w ? __builtin_amdgcn_readlane(rho_l, h - hbase)
+                                            : (int32_t)bounded(readlane64(wr2, h - hbase), (uint64_t)nf);
                 // a key below a fitting key fits too
                 for (int32_t pass = 1; pass <= rho; ++pass) {
                     const uint64_t prev = best;
@@ -715,14 +726,13 @@ __global__ void __launch_bounds__(64) k_pack_fit_reg(TrialArgs a, PackFast pf) {
                 }
                 c = 0xFFFF - (int32_t)(best & 0xFFFF);
             }
-            // c is uniform: only its chunk's owner lane changes (a uniform
-            // branch per chunk, so every register index stays static)
+            // c is uniform: only its chunk's owner lane changes (a select per
+            // chunk, so every register index stays static)
             const int32_t cu = c >> 6;
             const bool own = (c & (kWave - 1)) == lane;
-            const uint64_t add = ((uint64_t)(uint32_t)ti << 32) - ((uint64_t)1 << 16);
+            const uint64_t add = own ? ((uint64_t)(uint32_t)ti << 32) - ((uint64_t)1 << 16) : 0;
 #pragma unroll
-            for (int u = 0; u < NCH; ++u)
-                if (u == cu && own) kr[u] += add;
+            for (int u = 0; u < NCH; ++u) kr[u] += u == cu ? add : 0;
             if (lane == h - hbase) {
                 p_item = item;
                 p_cell = c;
