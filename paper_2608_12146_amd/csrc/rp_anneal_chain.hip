@@ -571,6 +571,11 @@ __device__ inline SlabPtrs slab_ptrs(const AnnealArgs &a, char *slab) {
 // index of every EDP shard, the shard of every slot, the slot count and slot
 // cells of every row-shard, and the lengths.
 // Every thread of the workgroup takes part (ends with a block barrier).
+// CG (the layout with the cell array and lengths in HBM) is a compile-time
+// choice so that the lengths pointer is known to be in LDS otherwise: a
+// pointer that may be either is read with flat loads, whose waits also wait
+// for every outstanding global store (a commit's W rows) before a screen.
+template <bool CG>
 __device__ inline Tables load_tables(const AnnealArgs &a, char *smem) {
     const int32_t N = a.N, D = a.D, G = a.G;
     int32_t *s_slots = reinterpret_cast<int32_t *>(smem);
@@ -599,7 +604,7 @@ __device__ inline Tables load_tables(const AnnealArgs &a, char *smem) {
         if (k == 0) s_hcnt[h] = cnt;
         if (hcell) s_hcell[x] = r * D + a.slots[g * D + (k < cnt ? k : cnt - 1)];
     }
-    if (a.cg) {  // the lengths are read from HBM (L2)
+    if constexpr (CG) {  // the lengths are read from HBM (L2)
         __syncthreads();
         return Tables{s_slots, s_count, s_shard, s_soff, a.t, s_hcnt, s_hcell};
     }
@@ -1275,7 +1280,7 @@ constexpr int kRunMaxWaves = 4;
 template <int PV, int DV, int GV, int LV, bool CG>
 __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain(AnnealArgs a) {
     extern __shared__ __align__(16) char smem[];
-    const Tables tb = load_tables(a, smem);
+    const Tables tb = load_tables<CG>(a, smem);
     const int wv = wave_id();
     const int m = blockIdx.x * a.mpw + wv;
     if (m >= a.pop) return;  // no block barrier follows
@@ -1560,7 +1565,7 @@ __global__ void __launch_bounds__(kRunMaxWaves * kWave) k_anneal_chain_run(Annea
     __shared__ uint64_t s_red[kRunMaxWaves];
     __shared__ double s_dred[kRunMaxWaves];
     __shared__ int32_t s_win, s_ok;
-    const Tables tb = load_tables(a, smem);
+    const Tables tb = load_tables<false>(a, smem);  // (never the CG layout)
     const int tid = threadIdx.x, nt = blockDim.x, lane = lane_id(), wv = wave_id(), nwv = nt / kWave;
     const int32_t pop = a.pop, N = a.N, K = a.K;
     const int gw = blockIdx.x * a.mpw + wv;  // this wave's slab
