@@ -75,10 +75,15 @@ def _code_text(src: str) -> str:
 
 
 def kernel_source_hash(kernel) -> str:
+    """SHA-256 of the kernel's sources (code only) and of the flags the
+    .hip ones compile with."""
+    from paper_2608_12146_amd import build as B
     h = hashlib.sha256()
     for f in kernel_sources(kernel):
         with open(f, encoding="utf-8") as fh:
             h.update(_code_text(fh.read()).encode())
+        if f.endswith(".hip"):
+            h.update(" ".join(B.flags_for(f)).encode())
     return h.hexdigest()[:16]
 
 
