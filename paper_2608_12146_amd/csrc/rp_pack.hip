@@ -405,20 +405,22 @@ __global__ void __launch_bounds__(64) k_pack_trials(TrialArgs a) {
 
 // ---------------------------------------------------------------------------
 // Seed trials in three launches for the common shapes (C < 2^31, N and K
-// below 2^16, the trial's W table within LDS); the single-kernel path above
-// covers the rest.  Same draws, same decisions.
+// below 2^16, the pairing's tables other than W within LDS); the
+// single-kernel path above covers the rest.  Same draws, same decisions.
 //
 //  k_pack_fit      one wave per candidate: WindowShuffle and
 //                  RandomizedBestFit with the draws, window items and their
 //                  lengths prefetched 64 steps ahead into lane registers; the
 //                  ranked pick compares 64-bit keys (load, then fewer
 //                  members, then lower index) with DPP maxima.  Ends with the
-//                  member list of every cell.
+//                  member list of every cell.  k_pack_fit_reg keeps the keys
+//                  in registers up to 2048 cells, k_pack_fit in LDS above.
 //  k_pack_cellsum  one workgroup per (candidate, cell): Q_k = sum of the
 //                  member rows and peak_k = sum_l max_p Q_k.
 //  k_pack_pair     one workgroup per candidate: EDPAwarePair with the W table
-//                  in LDS, threads over 4 consecutive entries of W + Q_k and a
-//                  DPP maximum over each layer's ranks, and the next cell's Q
+//                  in LDS when it fits (else in the trial's slice of HBM),
+//                  threads over 4 consecutive entries of W + Q_k and a DPP
+//                  maximum over each layer's ranks, and the next cell's Q
 //                  row prefetched during each step.
 
 struct PackFast {
