@@ -24,7 +24,10 @@
  *   call there (the stream orders the two); arenas are held until the
  *   process ends.  Scratch that does not fit the arena comes from the pool
  *   and goes back to it before the call returns (synchronous calls) or
- *   stream-ordered on `stream` (asynchronous calls).
+ *   stream-ordered on `stream` (asynchronous calls).  Arenas are keyed by
+ *   the stream handle: synchronize a stream before destroying it if library
+ *   work may still be pending on it, since a new stream can take the same
+ *   handle and with it the arena.
  * - Work is enqueued on the caller's `stream`.  Calls marked "synchronizes"
  *   wait for that stream before returning.  Results depend on the arguments
  *   only; calls on different streams are independent (each stream has its
