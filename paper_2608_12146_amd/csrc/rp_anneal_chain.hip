@@ -424,9 +424,11 @@ __device__ inline int32_t count_less_g(const int32_t *pool, int32_t lo, int32_t 
 // pool_move on an int32 pool in global memory (64 ranks): each batch loads
 // all of its entries before it stores any, and the batches walk in the
 // direction of the shift, so no load reads an entry an earlier batch wrote.
+// A batch is 2048 entries (32 per lane): a relocation across the pool of the
+// largest window shifts up to 32768 entries, one memory round trip a batch.
 __device__ inline void pool_move_g(int32_t *pool, int32_t from, int32_t to, int32_t v) {
     const int lane = lane_id();
-    constexpr int U = 8;
+    constexpr int U = 32;
     if (from < to) {
         // new[x] = old[x + 1] for from <= x < to
         for (int32_t base = from; base < to; base += U * kWave) {
